@@ -1,0 +1,148 @@
+/*
+ * cd.h -- C ABI of the MI355X (gfx950) batched Chamfer-distance library.
+ *
+ * Operation (Kaolin, Sec. 2.5: Chamfer distance for point clouds, defined
+ * through the cited point-set-generation paper of Fan et al.).  For clouds
+ * X [B,N,3] and Y [B,M,3] and the squared distance
+ *     d(p,q) = ((p.x-q.x)^2 + (p.y-q.y)^2) + (p.z-q.z)^2      (float32)
+ * the library computes, per item b,
+ *     dist_xy[b,i] = min_j d(x_i, y_j),  idx_xy[b,i] = lowest j attaining it
+ *     dist_yx[b,j] = min_i d(y_j, x_i),  idx_yx[b,j] = lowest i attaining it
+ *     chamfer[b]   = w1 * mean_i dist_xy[b,i] + w2 * mean_j dist_yx[b,j]
+ * the F-score at a distance threshold, and the gradient of the loss with
+ * respect to both clouds.  The squared distances are evaluated in float32 as
+ * fma(dz,dz, fma(dy,dy, dx*dx)) with d = query - target.
+ *
+ * Conventions shared by every call:
+ *  - Array pointers are DEVICE memory (hipMalloc or torch tensors on the
+ *    device), allocated and owned by the caller.  The library allocates no
+ *    memory, keeps no pointer after a call returns and holds no mutable
+ *    global state other than the thread-local error text and a per-device
+ *    cache of the compute-unit count.
+ *  - Layout: X and Y are float32, row-major, contiguous [B, N, 3] / [B, M, 3]
+ *    (x, y, z interleaved).  Per-point outputs are contiguous [B, N] / [B, M];
+ *    per-item outputs are [B].
+ *  - Every call is asynchronous on `stream` (NULL = the null stream).  CD_OK
+ *    means "enqueued"; results are valid once the stream has reached them.
+ *  - Arguments are checked before anything is enqueued, without touching
+ *    device memory: a NULL pointer (when B > 0), B < 0, N < 1, M < 1,
+ *    N or M >= 2^31 (indices are int32), a negative or NaN tau, or an
+ *    unaligned workspace returns CD_ERR_INVALID_ARG.  B == 0 is a no-op that
+ *    returns CD_OK.
+ *  - Inputs must be finite and their squared distances must not overflow;
+ *    other inputs are undefined behaviour.  Outputs must not alias inputs.
+ *  - A failed launch returns CD_ERR_HIP; cd_last_error() then holds the HIP
+ *    error text for the calling thread.
+ */
+#ifndef CD_H
+#define CD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t;
+
+typedef enum {
+    CD_OK = 0,
+    CD_ERR_INVALID_ARG = 1,
+    CD_ERR_WORKSPACE = 2,
+    CD_ERR_HIP = 3
+} cd_status;
+
+/* Static, human-readable name of a status code. */
+const char *cd_status_string(cd_status s);
+
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char *cd_last_error(void);
+
+/* Library version as "major.minor.patch" (static string). */
+const char *cd_version(void);
+
+/*
+ * Bytes of device workspace cd_forward needs for this shape (0 when B == 0).
+ * Returns 0 and sets cd_last_error() for an invalid shape.
+ */
+size_t cd_workspace_bytes(int64_t B, int64_t N, int64_t M);
+
+/*
+ * Nearest neighbours in both directions (Sec. 2.5: the point matching that
+ * the Chamfer distance is built on).
+ *   X [B,N,3], Y [B,M,3]      input clouds (device, float32)
+ *   dist_xy [B,N], idx_xy [B,N]   for every x_i: min_j d(x_i,y_j) and the
+ *                                 lowest j attaining it (float32 / int32)
+ *   dist_yx [B,M], idx_yx [B,M]   the same for every y_j against X
+ *   ws, ws_bytes               device workspace of at least
+ *                              cd_workspace_bytes(B,N,M) bytes, 256-byte
+ *                              aligned; its contents on entry are ignored and
+ *                              on exit are unspecified.  CD_ERR_WORKSPACE if
+ *                              too small.
+ * Results are bitwise reproducible from run to run.
+ */
+cd_status cd_forward(int64_t B, int64_t N, int64_t M,
+                     const float *X, const float *Y,
+                     float *dist_xy, int32_t *idx_xy,
+                     float *dist_yx, int32_t *idx_yx,
+                     void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Chamfer reduction (Sec. 2.5): chamfer[b] = w1 * (sum_i dist_xy[b,i]) / N
+ * + w2 * (sum_j dist_yx[b,j]) / M.  Sums are accumulated in double in a fixed
+ * order and the result rounded once to float32 (bitwise reproducible).
+ *   dist_xy [B,N], dist_yx [B,M]  from cd_forward;  chamfer [B] output.
+ */
+cd_status cd_reduce(int64_t B, int64_t N, int64_t M,
+                    const float *dist_xy, const float *dist_yx,
+                    float w1, float w2, float *chamfer, hipStream_t stream);
+
+/*
+ * F-score at threshold tau (a point-cloud metric beside the Chamfer distance
+ * in Sec. 2.5; the paper does not define it, the standard definition is
+ * used): a point is matched when its nearest-neighbour distance is strictly
+ * below tau, tested exactly as dist < tau^2 on the float32 squared distance.
+ *   precision[b] = #{i: dist_xy[b,i] < tau^2} / N
+ *   recall[b]    = #{j: dist_yx[b,j] < tau^2} / M
+ *   f[b]         = 2 P R / (P + R), or 0 when P + R == 0
+ * P, R and F are computed in double and rounded to float32.  `precision` and
+ * `recall` may be NULL; `f` may not.  tau < 0 or NaN is CD_ERR_INVALID_ARG.
+ */
+cd_status cd_fscore(int64_t B, int64_t N, int64_t M,
+                    const float *dist_xy, const float *dist_yx, float tau,
+                    float *f, float *precision, float *recall, hipStream_t stream);
+
+/*
+ * Backward of sum_b grad_out[b] * chamfer[b] (the Chamfer loss used to
+ * supervise networks, Sec. 2.5), for the neighbours cd_forward chose:
+ *   gX[b,i] = 2 g_xy (x_i - y_{idx_xy[i]}) - sum_{j: idx_yx[j]=i} 2 g_yx (y_j - x_i)
+ *   gY[b,j] = 2 g_yx (y_j - x_{idx_yx[j]}) - sum_{i: idx_xy[i]=j} 2 g_xy (x_i - y_j)
+ * with g_xy = grad_out[b] * w1 / N and g_yx = grad_out[b] * w2 / M.
+ *   grad_out [B]; X, Y, idx_xy, idx_yx as passed to / returned by cd_forward.
+ *   gX [B,N,3], gY [B,M,3] are fully overwritten (not accumulated).
+ * The scatter terms are added with float atomics, so the last bits may vary
+ * from run to run.  A point whose index lies outside [0, M) / [0, N)
+ * contributes nothing (its own and scatter terms are dropped).
+ */
+cd_status cd_backward(int64_t B, int64_t N, int64_t M, const float *grad_out,
+                      float w1, float w2, const float *X, const float *Y,
+                      const int32_t *idx_xy, const int32_t *idx_yx,
+                      float *gX, float *gY, hipStream_t stream);
+
+/*
+ * Backward for an arbitrary loss of the nearest-neighbour distances:
+ * g_xy [B,N] = dL/d dist_xy and g_yx [B,M] = dL/d dist_yx are given per point;
+ * gX, gY are as in cd_backward with those per-point factors.
+ */
+cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M,
+                                const float *g_xy, const float *g_yx,
+                                const float *X, const float *Y,
+                                const int32_t *idx_xy, const int32_t *idx_yx,
+                                float *gX, float *gY, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CD_H */

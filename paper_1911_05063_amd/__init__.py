@@ -1,0 +1,223 @@
+"""MI355X-native batched Chamfer distance (Kaolin, arXiv 1911.05063, Sec. 2.5).
+
+Thin Python binding over the C ABI of ``libcd_hip.so`` (declared in
+``include/cd.h``).  It only marshals arguments: torch supplies device memory
+and the current stream, every step of the computation runs in the library's
+HIP kernels.  There is no CPU fallback: if the library is missing or the
+tensors are not on a ROCm device, the calls raise.
+
+Functions (names follow the C ABI):
+  nn_distance(X, Y)                 -> dist_xy, idx_xy, dist_yx, idx_yx
+  chamfer_reduce(dist_xy, dist_yx)  -> chamfer [B]
+  f_score(dist_xy, dist_yx, tau)    -> f, precision, recall  [B] each
+  chamfer_backward(...)             -> gX, gY
+  chamfer_distance(X, Y, w1, w2)    -> chamfer [B], differentiable (autograd)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+__all__ = [
+    "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "chamfer_reduce",
+    "f_score", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
+    "ChamferDistance", "forward_step",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcd_hip.so")
+CD_OK = 0
+
+_lib = None
+
+
+class CDError(RuntimeError):
+    """A cd_* call returned a status other than CD_OK."""
+
+
+def library() -> ctypes.CDLL:
+    """Load libcd_hip.so (built in-tree by paper_1911_05063_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_1911_05063_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, vp, f32, st = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_int
+    lib.cd_status_string.restype = ctypes.c_char_p
+    lib.cd_status_string.argtypes = [st]
+    lib.cd_last_error.restype = ctypes.c_char_p
+    lib.cd_last_error.argtypes = []
+    lib.cd_version.restype = ctypes.c_char_p
+    lib.cd_version.argtypes = []
+    lib.cd_workspace_bytes.restype = ctypes.c_size_t
+    lib.cd_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.cd_forward.restype = st
+    lib.cd_forward.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.cd_reduce.restype = st
+    lib.cd_reduce.argtypes = [i64, i64, i64, vp, vp, f32, f32, vp, vp]
+    lib.cd_fscore.restype = st
+    lib.cd_fscore.argtypes = [i64, i64, i64, vp, vp, f32, vp, vp, vp, vp]
+    lib.cd_backward.restype = st
+    lib.cd_backward.argtypes = [i64, i64, i64, vp, f32, f32, vp, vp, vp, vp, vp, vp, vp]
+    lib.cd_backward_pointwise.restype = st
+    lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != CD_OK:
+        lib = library()
+        raise CDError(f"{what}: {lib.cd_status_string(status).decode()}: "
+                      f"{lib.cd_last_error().decode()}")
+
+
+def _device_tensor(t: torch.Tensor, name: str, dtype: torch.dtype) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a ROCm GPU (got {t.device}); there is no CPU path")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    return t.contiguous()
+
+
+def _cloud(t: torch.Tensor, name: str) -> torch.Tensor:
+    t = _device_tensor(t, name, torch.float32)
+    if t.dim() != 3 or t.shape[2] != 3:
+        raise ValueError(f"{name} must have shape [B, n, 3] (got {tuple(t.shape)})")
+    return t
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def workspace_bytes(B: int, N: int, M: int) -> int:
+    """Device workspace (bytes) that cd_forward needs for this shape."""
+    return int(library().cd_workspace_bytes(B, N, M))
+
+
+def nn_distance(X: torch.Tensor, Y: torch.Tensor, workspace: Optional[torch.Tensor] = None
+                ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Nearest neighbours both ways: (dist_xy [B,N], idx_xy [B,N], dist_yx [B,M], idx_yx [B,M])."""
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    if X.device != Y.device or X.shape[0] != Y.shape[0]:
+        raise ValueError("X and Y must share device and batch size")
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    dev = X.device
+    dist_xy = torch.empty((B, N), dtype=torch.float32, device=dev)
+    idx_xy = torch.empty((B, N), dtype=torch.int32, device=dev)
+    dist_yx = torch.empty((B, M), dtype=torch.float32, device=dev)
+    idx_yx = torch.empty((B, M), dtype=torch.int32, device=dev)
+    lib = library()
+    need = int(lib.cd_workspace_bytes(B, N, M))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    with torch.cuda.device(dev):
+        _check(lib.cd_forward(B, N, M, _ptr(X), _ptr(Y), _ptr(dist_xy), _ptr(idx_xy),
+                              _ptr(dist_yx), _ptr(idx_yx), _ptr(workspace), workspace.numel(),
+                              ctypes.c_void_p(_stream(dev))), "cd_forward")
+    return dist_xy, idx_xy, dist_yx, idx_yx
+
+
+def chamfer_reduce(dist_xy: torch.Tensor, dist_yx: torch.Tensor, w1: float = 1.0,
+                   w2: float = 1.0) -> torch.Tensor:
+    """chamfer[b] = w1 * mean_i dist_xy[b,i] + w2 * mean_j dist_yx[b,j]."""
+    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
+    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
+    out = torch.empty(B, dtype=torch.float32, device=dxy.device)
+    with torch.cuda.device(dxy.device):
+        _check(library().cd_reduce(B, N, M, _ptr(dxy), _ptr(dyx), float(w1), float(w2), _ptr(out),
+                                   ctypes.c_void_p(_stream(dxy.device))), "cd_reduce")
+    return out
+
+
+def f_score(dist_xy: torch.Tensor, dist_yx: torch.Tensor, tau: float):
+    """F-score@tau per item: (f, precision, recall), each [B] float32."""
+    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
+    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
+    f, p, r = (torch.empty(B, dtype=torch.float32, device=dxy.device) for _ in range(3))
+    with torch.cuda.device(dxy.device):
+        _check(library().cd_fscore(B, N, M, _ptr(dxy), _ptr(dyx), float(tau), _ptr(f), _ptr(p),
+                                   _ptr(r), ctypes.c_void_p(_stream(dxy.device))), "cd_fscore")
+    return f, p, r
+
+
+def chamfer_backward(grad_out: torch.Tensor, X: torch.Tensor, Y: torch.Tensor,
+                     idx_xy: torch.Tensor, idx_yx: torch.Tensor, w1: float = 1.0,
+                     w2: float = 1.0) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Gradient of sum_b grad_out[b] * chamfer[b] w.r.t. X and Y."""
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    go = _device_tensor(grad_out, "grad_out", torch.float32)
+    ixy = _device_tensor(idx_xy, "idx_xy", torch.int32)
+    iyx = _device_tensor(idx_yx, "idx_yx", torch.int32)
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    gX = torch.empty_like(X)
+    gY = torch.empty_like(Y)
+    with torch.cuda.device(X.device):
+        _check(library().cd_backward(B, N, M, _ptr(go), float(w1), float(w2), _ptr(X), _ptr(Y),
+                                     _ptr(ixy), _ptr(iyx), _ptr(gX), _ptr(gY),
+                                     ctypes.c_void_p(_stream(X.device))), "cd_backward")
+    return gX, gY
+
+
+def chamfer_backward_pointwise(g_xy: torch.Tensor, g_yx: torch.Tensor, X: torch.Tensor,
+                               Y: torch.Tensor, idx_xy: torch.Tensor, idx_yx: torch.Tensor
+                               ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Gradient w.r.t. X and Y given dL/d dist_xy [B,N] and dL/d dist_yx [B,M]."""
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    gxy = _device_tensor(g_xy, "g_xy", torch.float32)
+    gyx = _device_tensor(g_yx, "g_yx", torch.float32)
+    ixy = _device_tensor(idx_xy, "idx_xy", torch.int32)
+    iyx = _device_tensor(idx_yx, "idx_yx", torch.int32)
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    gX = torch.empty_like(X)
+    gY = torch.empty_like(Y)
+    with torch.cuda.device(X.device):
+        _check(library().cd_backward_pointwise(B, N, M, _ptr(gxy), _ptr(gyx), _ptr(X), _ptr(Y),
+                                               _ptr(ixy), _ptr(iyx), _ptr(gX), _ptr(gY),
+                                               ctypes.c_void_p(_stream(X.device))),
+               "cd_backward_pointwise")
+    return gX, gY
+
+
+class ChamferDistance(torch.autograd.Function):
+    """Per-item Chamfer distance with its backward through the HIP kernels."""
+
+    @staticmethod
+    def forward(ctx, X, Y, w1: float = 1.0, w2: float = 1.0):
+        dist_xy, idx_xy, dist_yx, idx_yx = nn_distance(X, Y)
+        ctx.save_for_backward(X, Y, idx_xy, idx_yx)
+        ctx.w = (float(w1), float(w2))
+        return chamfer_reduce(dist_xy, dist_yx, w1, w2)
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        X, Y, idx_xy, idx_yx = ctx.saved_tensors
+        gX, gY = chamfer_backward(grad_out.float(), X, Y, idx_xy, idx_yx, *ctx.w)
+        return gX, gY, None, None
+
+
+def chamfer_distance(X: torch.Tensor, Y: torch.Tensor, w1: float = 1.0, w2: float = 1.0
+                     ) -> torch.Tensor:
+    """Differentiable per-item Chamfer distance [B] (batch mean is the caller's)."""
+    return ChamferDistance.apply(X, Y, w1, w2)
+
+
+def forward_step(X, Y, taus=(0.01,), w1: float = 1.0, w2: float = 1.0, workspace=None):
+    """One forward pass of the whole path: neighbours, Chamfer, F-score at each tau."""
+    dist_xy, idx_xy, dist_yx, idx_yx = nn_distance(X, Y, workspace)
+    cd = chamfer_reduce(dist_xy, dist_yx, w1, w2)
+    fs = {float(t): f_score(dist_xy, dist_yx, t) for t in taus}
+    return dict(dist_xy=dist_xy, idx_xy=idx_xy, dist_yx=dist_yx, idx_yx=idx_yx, chamfer=cd,
+                fscore=fs)

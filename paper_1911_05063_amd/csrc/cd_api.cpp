@@ -1,0 +1,203 @@
+// C ABI of the batched Chamfer-distance library (declared in include/cd.h):
+// argument checking, workspace layout, launch planning and error reporting.
+// All device work is enqueued by the launchers in the .hip files.
+#include "cd.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+
+#include "cd_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+cd_status invalid(const char *what)
+{
+    std::snprintf(g_last_error, sizeof(g_last_error), "invalid argument: %s", what);
+    return CD_ERR_INVALID_ARG;
+}
+
+cd_status hip_failed(hipError_t e, const char *where)
+{
+    std::snprintf(g_last_error, sizeof(g_last_error), "%s: %s (%d)", where, hipGetErrorString(e),
+                  static_cast<int>(e));
+    return CD_ERR_HIP;
+}
+
+constexpr int64_t kMaxPoints = 2147483647LL;  // indices are int32
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+// Compute units of the current device, cached per device.
+cd_status current_cu_count(int *out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_failed(e, "hipGetDevice");
+    if (dev >= 0 && dev < kMaxDevices) {
+        const int cached = g_cu_count[dev].load(std::memory_order_relaxed);
+        if (cached > 0) {
+            *out = cached;
+            return CD_OK;
+        }
+    }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_failed(e, "hipDeviceGetAttribute");
+    if (cus < 1) cus = 1;
+    if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(cus, std::memory_order_relaxed);
+    *out = cus;
+    return CD_OK;
+}
+
+// Shape checks shared by every entry point.
+cd_status check_shape(int64_t B, int64_t N, int64_t M)
+{
+    if (B < 0) return invalid("B < 0");
+    if (N < 1) return invalid("N < 1 (nearest neighbour over an empty cloud is undefined)");
+    if (M < 1) return invalid("M < 1 (nearest neighbour over an empty cloud is undefined)");
+    if (N > kMaxPoints || M > kMaxPoints) return invalid("N or M >= 2^31 (indices are int32)");
+    // Flattened per-thread indices (backward) and work items must fit the launch grid.
+    if (B > 0 && (B > (int64_t(1) << 40) / (N + M)))
+        return invalid("B * (N + M) too large for one launch");
+    return CD_OK;
+}
+
+bool aligned256(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *cd_status_string(cd_status s)
+{
+    switch (s) {
+    case CD_OK: return "CD_OK";
+    case CD_ERR_INVALID_ARG: return "CD_ERR_INVALID_ARG";
+    case CD_ERR_WORKSPACE: return "CD_ERR_WORKSPACE";
+    case CD_ERR_HIP: return "CD_ERR_HIP";
+    }
+    return "CD_UNKNOWN_STATUS";
+}
+
+const char *cd_last_error(void) { return g_last_error; }
+
+const char *cd_version(void) { return "0.1.0"; }
+
+size_t cd_workspace_bytes(int64_t B, int64_t N, int64_t M)
+{
+    if (check_shape(B, N, M) != CD_OK) return 0;
+    if (B == 0) return 0;
+    return cdk::workspace_layout(B, N, M).total;
+}
+
+cd_status cd_forward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                     float *dist_xy, int32_t *idx_xy, float *dist_yx, int32_t *idx_yx, void *ws,
+                     size_t ws_bytes, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!X || !Y || !dist_xy || !idx_xy || !dist_yx || !idx_yx) return invalid("NULL array pointer");
+    const cdk::WsLayout lay = cdk::workspace_layout(B, N, M);
+    if (!ws || ws_bytes < lay.total) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, lay.total);
+        return CD_ERR_WORKSPACE;
+    }
+    if (!aligned256(ws)) return invalid("workspace not 256-byte aligned");
+
+    int cus = 0;
+    s = current_cu_count(&cus);
+    if (s != CD_OK) return s;
+    cdk::NNPlan plan;
+    cdk::make_plan(plan, B, N, M, cus);
+    if (plan.d[0].items + plan.d[1].items > 2147483647LL)
+        return invalid("too many work items for one launch");
+    char *w = static_cast<char *>(ws);
+    plan.d[0].P = X;
+    plan.d[0].Q = Y;
+    plan.d[0].dist = dist_xy;
+    plan.d[0].idx = idx_xy;
+    plan.d[0].keys = reinterpret_cast<unsigned long long *>(w + lay.keys_xy);
+    plan.d[1].P = Y;
+    plan.d[1].Q = X;
+    plan.d[1].dist = dist_yx;
+    plan.d[1].idx = idx_yx;
+    plan.d[1].keys = reinterpret_cast<unsigned long long *>(w + lay.keys_yx);
+    const hipError_t e = cdk::launch_forward(plan, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_forward launch");
+    return CD_OK;
+}
+
+cd_status cd_reduce(int64_t B, int64_t N, int64_t M, const float *dist_xy, const float *dist_yx,
+                    float w1, float w2, float *chamfer, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!dist_xy || !dist_yx || !chamfer) return invalid("NULL array pointer");
+    const hipError_t e = cdk::launch_reduce(B, N, M, dist_xy, dist_yx, static_cast<double>(w1),
+                                            static_cast<double>(w2), chamfer, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_reduce launch");
+    return CD_OK;
+}
+
+cd_status cd_fscore(int64_t B, int64_t N, int64_t M, const float *dist_xy, const float *dist_yx,
+                    float tau, float *f, float *precision, float *recall, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (std::isnan(tau) || tau < 0.0f) return invalid("tau must be >= 0 and not NaN");
+    if (B == 0) return CD_OK;
+    if (!dist_xy || !dist_yx || !f) return invalid("NULL array pointer");
+    // A float32 squared distance d satisfies d < tau^2 (exact in double) iff
+    // d < thr, where thr is the smallest float32 >= tau^2.
+    const double t2 = static_cast<double>(tau) * static_cast<double>(tau);
+    float thr = static_cast<float>(t2);
+    if (static_cast<double>(thr) < t2) thr = std::nextafter(thr, INFINITY);
+    const hipError_t e =
+        cdk::launch_fscore(B, N, M, dist_xy, dist_yx, thr, f, precision, recall, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_fscore launch");
+    return CD_OK;
+}
+
+cd_status cd_backward(int64_t B, int64_t N, int64_t M, const float *grad_out, float w1, float w2,
+                      const float *X, const float *Y, const int32_t *idx_xy,
+                      const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!grad_out || !X || !Y || !idx_xy || !idx_yx || !gX || !gY)
+        return invalid("NULL array pointer");
+    const float sxy = static_cast<float>(static_cast<double>(w1) / static_cast<double>(N));
+    const float syx = static_cast<float>(static_cast<double>(w2) / static_cast<double>(M));
+    const hipError_t e = cdk::launch_backward(B, N, M, grad_out, grad_out, false, sxy, syx, X, Y,
+                                              idx_xy, idx_yx, gX, gY, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_backward launch");
+    return CD_OK;
+}
+
+cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M, const float *g_xy,
+                                const float *g_yx, const float *X, const float *Y,
+                                const int32_t *idx_xy, const int32_t *idx_yx, float *gX,
+                                float *gY, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!g_xy || !g_yx || !X || !Y || !idx_xy || !idx_yx || !gX || !gY)
+        return invalid("NULL array pointer");
+    const hipError_t e = cdk::launch_backward(B, N, M, g_xy, g_yx, true, 1.0f, 1.0f, X, Y, idx_xy,
+                                              idx_yx, gX, gY, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_backward_pointwise launch");
+    return CD_OK;
+}
+
+}  // extern "C"

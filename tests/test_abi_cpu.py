@@ -1,0 +1,144 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/cd.h declares, and rejects bad arguments before it
+enqueues anything (these calls never reach the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cd.h")
+
+CD_OK, CD_ERR_INVALID_ARG, CD_ERR_WORKSPACE, CD_ERR_HIP = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_1911_05063_amd as cd
+    if not os.path.exists(cd.LIB_PATH):
+        from paper_1911_05063_amd import build
+        build.build()
+    return cd.library()
+
+
+def declared_functions():
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cd_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_path():
+    names = declared_functions()
+    for n in ("cd_forward", "cd_reduce", "cd_fscore", "cd_backward", "cd_backward_pointwise",
+              "cd_workspace_bytes", "cd_status_string", "cd_last_error", "cd_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in cd.h but not exported"
+
+
+def test_exported_symbols_are_unmangled_c():
+    import subprocess
+    import paper_1911_05063_amd as cd
+    out = subprocess.run(["nm", "-D", "--defined-only", cd.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    for name in declared_functions():
+        assert name in exported
+
+
+def test_status_strings(lib):
+    assert lib.cd_status_string(CD_OK) == b"CD_OK"
+    assert lib.cd_status_string(CD_ERR_INVALID_ARG) == b"CD_ERR_INVALID_ARG"
+    assert lib.cd_status_string(CD_ERR_WORKSPACE) == b"CD_ERR_WORKSPACE"
+    assert lib.cd_status_string(CD_ERR_HIP) == b"CD_ERR_HIP"
+    assert lib.cd_version().count(b".") == 2
+
+
+def test_workspace_bytes(lib):
+    ws = lib.cd_workspace_bytes(16, 16384, 16384)
+    assert ws >= 8 * 16 * (16384 + 16384) and ws % 256 == 0
+    assert lib.cd_workspace_bytes(0, 10, 10) == 0
+    assert lib.cd_workspace_bytes(1, 0, 10) == 0
+    assert lib.cd_workspace_bytes(-1, 10, 10) == 0
+    assert lib.cd_workspace_bytes(1, 2 ** 31, 10) == 0
+    assert lib.cd_workspace_bytes(3, 7, 5) >= 8 * 3 * 12
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails its checks
+
+
+def fwd(lib, B, N, M, ptrs=(FAKE,) * 6, ws=FAKE, ws_bytes=1 << 30):
+    return lib.cd_forward(B, N, M, *ptrs, ws, ws_bytes, None)
+
+
+def test_forward_rejects_bad_shapes(lib):
+    assert fwd(lib, -1, 4, 4) == CD_ERR_INVALID_ARG
+    assert fwd(lib, 1, 0, 4) == CD_ERR_INVALID_ARG
+    assert fwd(lib, 1, 4, 0) == CD_ERR_INVALID_ARG
+    assert fwd(lib, 1, 2 ** 31, 4) == CD_ERR_INVALID_ARG
+    assert fwd(lib, 1, 4, 2 ** 31) == CD_ERR_INVALID_ARG
+    assert b"invalid argument" in lib.cd_last_error()
+
+
+def test_forward_rejects_null_pointers(lib):
+    for k in range(6):
+        ptrs = [FAKE] * 6
+        ptrs[k] = None
+        assert fwd(lib, 2, 4, 4, ptrs=tuple(ptrs)) == CD_ERR_INVALID_ARG
+    # B == 0 is a no-op even with NULL pointers.
+    assert fwd(lib, 0, 4, 4, ptrs=(None,) * 6, ws=None, ws_bytes=0) == CD_OK
+
+
+def test_forward_checks_workspace(lib):
+    need = lib.cd_workspace_bytes(2, 100, 50)
+    assert fwd(lib, 2, 100, 50, ws_bytes=need - 1) == CD_ERR_WORKSPACE
+    assert b"workspace too small" in lib.cd_last_error()
+    assert fwd(lib, 2, 100, 50, ws=None) == CD_ERR_WORKSPACE
+    assert fwd(lib, 2, 100, 50, ws=ctypes.c_void_p(0x1010)) == CD_ERR_INVALID_ARG  # unaligned
+
+
+def test_reduce_fscore_backward_reject_bad_args(lib):
+    assert lib.cd_reduce(1, 0, 3, FAKE, FAKE, 1.0, 1.0, FAKE, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_reduce(1, 3, 3, None, FAKE, 1.0, 1.0, FAKE, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_reduce(0, 3, 3, None, None, 1.0, 1.0, None, None) == CD_OK
+    assert lib.cd_fscore(1, 3, 3, FAKE, FAKE, -0.5, FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_fscore(1, 3, 3, FAKE, FAKE, float("nan"), FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_fscore(1, 3, 3, FAKE, FAKE, 0.1, None, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_fscore(0, 3, 3, None, None, 0.1, None, None, None, None) == CD_OK
+    args = [FAKE] * 7
+    for k in range(7):
+        a = list(args)
+        a[k] = None
+        go, X, Y, ixy, iyx, gX, gY = a
+        assert lib.cd_backward(1, 3, 3, go, 1.0, 1.0, X, Y, ixy, iyx, gX, gY, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_backward(-2, 3, 3, *([FAKE] * 1), 1.0, 1.0, *([FAKE] * 6), None) == CD_ERR_INVALID_ARG
+    for k in range(8):
+        a = [FAKE] * 8
+        a[k] = None
+        assert lib.cd_backward_pointwise(1, 3, 3, *a, None) == CD_ERR_INVALID_ARG
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    import paper_1911_05063_amd as cd
+    X = torch.zeros(1, 4, 3)
+    with pytest.raises(ValueError, match="ROCm GPU"):
+        cd.nn_distance(X, X)
+    with pytest.raises(ValueError, match="ROCm GPU"):
+        cd.chamfer_distance(X, X)
+
+
+def test_product_path_does_not_touch_the_oracle():
+    # The package sources never import, load or execute anything under oracle/.
+    pkg = os.path.join(ROOT, "paper_1911_05063_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".h")):
+                with open(os.path.join(dirpath, fn)) as f:
+                    src = f.read()
+                assert "oracle" not in src.replace("oracle-free", ""), fn

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Small and medium cases are compared element by element; the five full-size
+workloads are compared on sampled queries the oracle computes one by one,
+on the whole-array reductions, and on closed forms that hold at any size.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import gpu_checks as gc
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm GPU visible")
+    import paper_1911_05063_amd as cd
+    # The product path must be the HIP library: fail loudly if it is not built.
+    assert os.path.exists(cd.LIB_PATH), "libcd_hip.so missing: build before running GPU tests"
+    cd.library()
+    yield
+
+
+import paper_1911_05063_amd as cd  # noqa: E402
+
+# (kind, B, N, M, seed): ragged sizes that span several query blocks (512),
+# several sub-tiles (32) and target splits, plus the degenerate N=1 / M=1.
+SMALL_CASES = [
+    ("uniform", 1, 1024, 1024, 1),
+    ("uniform", 2, 1000, 1500, 2),
+    ("sphere", 3, 513, 2049, 3),
+    ("mesh", 2, 2048, 2048, 4),
+    ("gmm", 2, 3001, 700, 5),
+    ("grid_dup", 2, 1500, 1500, 6),
+    ("uniform", 1, 1, 77, 7),
+    ("uniform", 2, 77, 1, 8),
+    ("uniform", 1, 1, 1, 9),
+    ("mesh", 1, 31, 33, 10),
+    ("gmm", 1, 6000, 90, 11),
+    ("sphere", 5, 200, 4500, 12),
+]
+
+
+def _case_id(c):
+    return f"{c[0]}-B{c[1]}-N{c[2]}-M{c[3]}"
+
+
+@pytest.mark.parametrize("case", SMALL_CASES, ids=_case_id)
+def test_forward_matches_oracle(case):
+    kind, B, N, M, seed = case
+    X, Y = synth.generate(kind, B, N, M, seed)
+    print(f"[parity] {_case_id(case)}", flush=True)
+    g = gc.gpu_forward(X, Y)
+    gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), _case_id(case))
+    r = oracle.nn(X, Y, fused=False)
+    gc.assert_nn_unfused(X, Y, g[0], g[1], r[0], r[1])
+    gc.assert_nn_unfused(Y, X, g[2], g[3], r[2], r[3])
+
+
+@pytest.mark.parametrize("case", SMALL_CASES[:6], ids=_case_id)
+def test_reduce_fscore_backward_match_oracle(case):
+    kind, B, N, M, seed = case
+    X, Y = synth.generate(kind, B, N, M, seed)
+    print(f"[parity-all] {_case_id(case)}", flush=True)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    w1, w2 = 0.75, 1.25
+    ch = gc.to_np(cd.chamfer_reduce(dxy, dyx, w1, w2))
+    dxy_n, dyx_n = gc.to_np(dxy), gc.to_np(dyx)
+    gc.assert_chamfer(ch, dxy_n, dyx_n, w1, w2)
+    for tau in (0.005, 0.01, 0.02, 0.1):
+        f, p, r = (gc.to_np(t) for t in cd.f_score(dxy, dyx, tau))
+        gc.assert_fscore(f, p, r, dxy_n, dyx_n, tau)
+    go = np.linspace(0.5, 2.0, B).astype(np.float32)
+    gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx, w1, w2)
+    gc.assert_grad(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx), go, w1, w2)
+
+
+def test_backward_pointwise_matches_oracle():
+    X, Y = synth.generate("grid_dup", 2, 900, 1100, 21)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    rng = np.random.default_rng(3)
+    g_xy = rng.standard_normal((2, 900)).astype(np.float32)
+    g_yx = rng.standard_normal((2, 1100)).astype(np.float32)
+    gX, gY = cd.chamfer_backward_pointwise(gc.to_gpu(g_xy), gc.to_gpu(g_yx), Xg, Yg, ixy, iyx)
+    rX, rY, sX, sY, nX, nY = oracle.backward_pointwise(g_xy, g_yx, X, Y, gc.to_np(ixy), gc.to_np(iyx))
+    for g, r, s, n in ((gc.to_np(gX), rX, sX, nX), (gc.to_np(gY), rY, sY, nY)):
+        tol = 1e-4 * np.abs(r) + 4.0 * (n[..., None] + 2) * gc.U32 * s
+        assert np.all(np.abs(g - r) <= tol)
+
+
+def test_autograd_chamfer_distance():
+    X, Y = synth.generate("mesh", 3, 700, 900, 31)
+    Xg = gc.to_gpu(X).requires_grad_(True)
+    Yg = gc.to_gpu(Y).requires_grad_(True)
+    out = cd.chamfer_distance(Xg, Yg, 1.0, 1.0)
+    weights = torch.tensor([1.0, -2.0, 0.5], device="cuda:0")
+    (out * weights).sum().backward()
+    dxy, ixy, dyx, iyx = oracle.nn(X, Y, fused=True)
+    gc.assert_chamfer(gc.to_np(out), dxy, dyx)
+    gc.assert_grad(gc.to_np(Xg.grad), gc.to_np(Yg.grad), X, Y, ixy, iyx,
+                   np.array([1.0, -2.0, 0.5]))
+
+
+def test_forward_is_bitwise_reproducible():
+    X, Y = synth.generate("grid_dup", 4, 4096, 3000, 41)
+    a = gc.gpu_forward(X, Y)
+    b = gc.gpu_forward(X, Y)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_symmetry_swaps_directions_bitwise():
+    X, Y = synth.generate("gmm", 2, 2500, 1800, 42)
+    a = gc.gpu_forward(X, Y)
+    b = gc.gpu_forward(Y, X)
+    assert np.array_equal(a[0], b[2]) and np.array_equal(a[1], b[3])
+    assert np.array_equal(a[2], b[0]) and np.array_equal(a[3], b[1])
+
+
+def test_identical_points_tie_to_lowest_index():
+    # Every target at the same place: every distance is equal, index 0 wins.
+    X = np.full((2, 700, 3), 0.25, np.float32)
+    Y = np.full((2, 1300, 3), -0.5, np.float32)
+    g = gc.gpu_forward(X, Y)
+    assert np.all(g[1] == 0) and np.all(g[3] == 0)
+    assert np.all(g[0] == np.float32(3 * 0.75 ** 2)) and np.all(g[2] == g[0][0, 0])
+
+
+def test_duplicates_across_splits_tie_to_lowest_index():
+    # Targets repeated many times along the cloud (so copies fall in different
+    # sub-tiles and target splits): the first copy must win everywhere.
+    X, Y0 = synth.generate("grid_dup", 2, 600, 300, 43)
+    Y = np.concatenate([Y0] * 40, axis=1)  # M = 12000
+    g = gc.gpu_forward(X, Y)
+    ref = oracle.nn(X, Y, fused=True)
+    gc.assert_nn_bitwise(g, ref, "dup")
+    assert np.all(g[1] < 300)
+
+
+def test_empty_batch_is_noop():
+    X = torch.empty((0, 5, 3), dtype=torch.float32, device="cuda:0")
+    Y = torch.empty((0, 7, 3), dtype=torch.float32, device="cuda:0")
+    dxy, ixy, dyx, iyx = cd.nn_distance(X, Y)
+    assert dxy.shape == (0, 5) and dyx.shape == (0, 7)
+    assert cd.chamfer_reduce(dxy, dyx).shape == (0,)
+
+
+def test_small_workspace_is_rejected():
+    import ctypes
+    lib = cd.library()
+    X = torch.zeros((1, 10, 3), device="cuda:0")
+    out = [torch.empty((1, 10), device="cuda:0") for _ in range(2)]
+    idx = [torch.empty((1, 10), dtype=torch.int32, device="cuda:0") for _ in range(2)]
+    ws = torch.empty(64, dtype=torch.uint8, device="cuda:0")
+    st = lib.cd_forward(1, 10, 10, X.data_ptr(), X.data_ptr(), out[0].data_ptr(), idx[0].data_ptr(),
+                        out[1].data_ptr(), idx[1].data_ptr(), ws.data_ptr(), 64, None)
+    assert st == 2 and b"workspace" in lib.cd_last_error()
+
+
+# ---------------------------------------------------------------- full size
+def _sample_rows(rng, B, n, count):
+    return np.stack([rng.integers(0, B, count), rng.integers(0, n, count)], axis=1)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_full_size_workload(k):
+    """Workload k at its full size, in the launch configuration the benchmark
+    times: sampled queries against the oracle (bitwise, same precision),
+    whole-array Chamfer / F-score / gradients against the oracle fed the
+    GPU's own neighbours, and the gradient identities."""
+    w = synth.WORKLOADS[k]
+    print(f"[full] {w.describe()}", flush=True)
+    X, Y = synth.workload(k)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    ch = cd.chamfer_reduce(dxy, dyx)
+    go = np.linspace(1.0, 2.0, w.B).astype(np.float32)
+    gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    fs = {t: cd.f_score(dxy, dyx, t) for t in w.taus}
+    torch.cuda.synchronize()
+    dxy_n, ixy_n, dyx_n, iyx_n = (gc.to_np(t) for t in (dxy, ixy, dyx, iyx))
+    rng = np.random.default_rng(1000 + k)
+    count = 1024 if k != 5 else 384
+    for P, Q, dist, idx, n in ((X, Y, dxy_n, ixy_n, w.N), (Y, X, dyx_n, iyx_n, w.M)):
+        rows = _sample_rows(rng, w.B, n, count)
+        rd, ri = gc.sample_nn(P, Q, rows, fused=True)
+        assert np.array_equal(dist[rows[:, 0], rows[:, 1]], rd)
+        assert np.array_equal(idx[rows[:, 0], rows[:, 1]], ri)
+    assert ixy_n.min() >= 0 and ixy_n.max() < w.M and iyx_n.min() >= 0 and iyx_n.max() < w.N
+    gc.assert_chamfer(gc.to_np(ch), dxy_n, dyx_n)
+    for t, (f, p, r) in fs.items():
+        gc.assert_fscore(gc.to_np(f), gc.to_np(p), gc.to_np(r), dxy_n, dyx_n, t)
+    gXn, gYn = gc.to_np(gX), gc.to_np(gY)
+    gc.assert_grad(gXn, gYn, X, Y, ixy_n, iyx_n, go)
+    gc.gradient_identities(gXn, gYn, X, Y, go, oracle.chamfer(dxy_n, dyx_n))
+
+
+@pytest.mark.parametrize("B,dims", [(16, (32, 32, 16)), (8, (64, 64, 16))],
+                         ids=["b16_n16384", "b8_n65536"])
+def test_lattice_closed_form_full_size(B, dims):
+    """Y = permuted (X + s) on a dyadic lattice at the full workload shapes:
+    every distance is |s|^2, neighbours follow the permutation, Chamfer is
+    2|s|^2 and gradients are -/+ 2 s (1/N + 1/M), all exactly (no oracle)."""
+    h, s = 1.0 / 16, np.array([1 / 64, -3 / 256, 1 / 128])
+    X, Y, perm = synth.lattice_pair(B, dims, h, s, seed=77)
+    N = X.shape[1]
+    s2 = np.float32((s ** 2).sum())
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    ch = cd.chamfer_reduce(dxy, dyx)
+    gX, gY = cd.chamfer_backward(torch.ones(B, device="cuda:0"), Xg, Yg, ixy, iyx)
+    f, _, _ = cd.f_score(dxy, dyx, float(np.sqrt(s2)) * 1.01)
+    torch.cuda.synchronize()
+    assert np.all(gc.to_np(dxy) == s2) and np.all(gc.to_np(dyx) == s2)
+    assert np.array_equal(gc.to_np(ixy), perm)
+    inv = np.empty_like(perm)
+    for b in range(B):
+        inv[b, perm[b]] = np.arange(N)
+    assert np.array_equal(gc.to_np(iyx), inv)
+    assert np.all(gc.to_np(ch) == np.float32(2 * s2))
+    k = 2.0 * (2.0 / N)
+    assert np.array_equal(gc.to_np(gX), np.broadcast_to((-k * s).astype(np.float32), X.shape))
+    assert np.array_equal(gc.to_np(gY), np.broadcast_to((k * s).astype(np.float32), Y.shape))
+    assert np.all(gc.to_np(f) == 1.0)
