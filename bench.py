@@ -10,8 +10,9 @@ F-score at tau = 0.005, 0.01, 0.02.
 
 Throughput is credited 2*B*N*M directed pair-evaluations per step (one per
 query/target pair in each direction).  The roofline object prices the
-dominant kernel (the nearest-neighbour search, timed with HIP events around
-every cd_forward call on the launch stream) at 9 FP32 operations per directed
+dominant call (cd_forward: the fused nearest-neighbour search kernel and its
+merge kernel, timed with HIP events around every cd_forward call on the launch
+stream) at 9 FP32 operations per directed
 pair-evaluation against the MI355X FP32 vector peak of 157.3 TFLOP/s.
 
 Prints ONE JSON line.  Single GPU only.
@@ -203,7 +204,7 @@ def main():
                         "fwd_bwd": ms_per_step},
         "pct_fp32_valu_peak": 100.0 * FLOPS_PER_PAIR * value / (PEAK_FP32_TFLOPS * 1e12),
         "wall_s": wall,
-        "roofline": {"bound": "alu", "kernel": "nn_search (cd_forward)",
+        "roofline": {"bound": "alu", "kernel": "cd_forward (search_kernel + merge_kernel)",
                      "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
                      "work_per_launch": f"{FLOPS_PER_PAIR} flop x {pairs:.4g} directed pair-evals"},

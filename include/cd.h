@@ -17,8 +17,7 @@
  *  - Array pointers are DEVICE memory (hipMalloc or torch tensors on the
  *    device), allocated and owned by the caller.  The library allocates no
  *    memory, keeps no pointer after a call returns and holds no mutable
- *    global state other than the thread-local error text and a per-device
- *    cache of the compute-unit count.
+ *    global state other than the thread-local error text.
  *  - Layout: X and Y are float32, row-major, contiguous [B, N, 3] / [B, M, 3]
  *    (x, y, z interleaved).  Per-point outputs are contiguous [B, N] / [B, M];
  *    per-item outputs are [B].

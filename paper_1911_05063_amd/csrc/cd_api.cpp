@@ -5,7 +5,6 @@
 
 #include <hip/hip_runtime_api.h>
 
-#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -30,30 +29,6 @@ cd_status hip_failed(hipError_t e, const char *where)
 }
 
 constexpr int64_t kMaxPoints = 2147483647LL;  // indices are int32
-constexpr int kMaxDevices = 64;
-std::atomic<int> g_cu_count[kMaxDevices];
-
-// Compute units of the current device, cached per device.
-cd_status current_cu_count(int *out)
-{
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return hip_failed(e, "hipGetDevice");
-    if (dev >= 0 && dev < kMaxDevices) {
-        const int cached = g_cu_count[dev].load(std::memory_order_relaxed);
-        if (cached > 0) {
-            *out = cached;
-            return CD_OK;
-        }
-    }
-    int cus = 0;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return hip_failed(e, "hipDeviceGetAttribute");
-    if (cus < 1) cus = 1;
-    if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(cus, std::memory_order_relaxed);
-    *out = cus;
-    return CD_OK;
-}
 
 // Shape checks shared by every entry point.
 cd_status check_shape(int64_t B, int64_t N, int64_t M)
@@ -93,7 +68,7 @@ size_t cd_workspace_bytes(int64_t B, int64_t N, int64_t M)
 {
     if (check_shape(B, N, M) != CD_OK) return 0;
     if (B == 0) return 0;
-    return cdk::workspace_layout(B, N, M).total;
+    return cdk::forward_workspace_bytes(cdk::plan_forward(B, N, M));
 }
 
 cd_status cd_forward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
@@ -104,33 +79,17 @@ cd_status cd_forward(int64_t B, int64_t N, int64_t M, const float *X, const floa
     if (s != CD_OK) return s;
     if (B == 0) return CD_OK;
     if (!X || !Y || !dist_xy || !idx_xy || !dist_yx || !idx_yx) return invalid("NULL array pointer");
-    const cdk::WsLayout lay = cdk::workspace_layout(B, N, M);
-    if (!ws || ws_bytes < lay.total) {
+    const cdk::FwdPlan plan = cdk::plan_forward(B, N, M);
+    const size_t need = cdk::forward_workspace_bytes(plan);
+    if (!ws || ws_bytes < need) {
         std::snprintf(g_last_error, sizeof(g_last_error),
-                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, lay.total);
+                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
         return CD_ERR_WORKSPACE;
     }
     if (!aligned256(ws)) return invalid("workspace not 256-byte aligned");
-
-    int cus = 0;
-    s = current_cu_count(&cus);
-    if (s != CD_OK) return s;
-    cdk::NNPlan plan;
-    cdk::make_plan(plan, B, N, M, cus);
-    if (plan.d[0].items + plan.d[1].items > 2147483647LL)
-        return invalid("too many work items for one launch");
-    char *w = static_cast<char *>(ws);
-    plan.d[0].P = X;
-    plan.d[0].Q = Y;
-    plan.d[0].dist = dist_xy;
-    plan.d[0].idx = idx_xy;
-    plan.d[0].keys = reinterpret_cast<unsigned long long *>(w + lay.keys_xy);
-    plan.d[1].P = Y;
-    plan.d[1].Q = X;
-    plan.d[1].dist = dist_yx;
-    plan.d[1].idx = idx_yx;
-    plan.d[1].keys = reinterpret_cast<unsigned long long *>(w + lay.keys_yx);
-    const hipError_t e = cdk::launch_forward(plan, stream);
+    if (cdk::forward_tiles(plan) > 2147483647LL) return invalid("too many tiles for one launch");
+    const cdk::FwdArgs args{X, Y, dist_xy, idx_xy, dist_yx, idx_yx, ws};
+    const hipError_t e = cdk::launch_forward(plan, args, stream);
     if (e != hipSuccess) return hip_failed(e, "cd_forward launch");
     return CD_OK;
 }

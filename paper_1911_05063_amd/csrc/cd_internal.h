@@ -8,45 +8,36 @@
 
 namespace cdk {
 
-// Sub-tile length of the deferred argmin: the search keeps, per query, only
-// the running minimum and the first target of the sub-tile that last lowered
-// it; the exact lowest index is recovered by rescanning that sub-tile.
-constexpr int kSubTile = 32;
-// Queries held in registers by each lane of the search kernel.
-constexpr int kQueriesPerLane = 8;
 constexpr int kWave = 64;
 
-// One search direction: queries P against targets Q (both [B, n, 3] float32).
-struct NNDir {
-    const float *P;
-    const float *Q;
-    float *dist;                 // [B, NP]   written when nsplit == 1
-    int32_t *idx;                // [B, NP]   written when nsplit == 1
-    unsigned long long *keys;    // [B, NP]   merged with atomicMin when nsplit > 1
-    int32_t NP, NQ;
-    int32_t nqb;                 // query blocks (kWave * kQueriesPerLane queries) per item
-    int32_t nsplit;              // target splits per item
-    int32_t chunk;               // targets per split, a multiple of kSubTile
-    int32_t pad;
-    int64_t items;               // B * nqb * nsplit work items (one wave each)
-};
-
-struct NNPlan {
-    NNDir d[2];
+// Tiling of the fused nearest-neighbour search (nn_search.hip).  The X cloud
+// is cut into query groups (rows), the Y cloud into target blocks (columns);
+// one workgroup computes every distance of one (item, group, block) tile.
+struct FwdPlan {
     int64_t B;
+    int32_t N, M;
+    int32_t nQG;   // query groups per item
+    int32_t nTB;   // target blocks per item
+    int32_t TB;    // targets per block (a multiple of the batch length)
 };
 
-// Layout of the forward workspace: the packed (distance, index) merge keys
-// of both directions, each segment 256-byte aligned.
-struct WsLayout {
-    size_t keys_xy, keys_yx, total;
+struct FwdArgs {
+    const float *X;      // [B, N, 3]
+    const float *Y;      // [B, M, 3]
+    float *dist_xy;      // [B, N]
+    int32_t *idx_xy;     // [B, N]
+    float *dist_yx;      // [B, M]
+    int32_t *idx_yx;     // [B, M]
+    void *ws;            // forward_workspace_bytes(plan) bytes, 256-byte aligned
 };
-WsLayout workspace_layout(int64_t B, int64_t N, int64_t M);
 
-// Fill `plan` for the given shape on a device with `cu_count` compute units.
-void make_plan(NNPlan &plan, int64_t B, int64_t N, int64_t M, int cu_count);
+// The plan depends on the shape only, so the workspace size does too.
+FwdPlan plan_forward(int64_t B, int64_t N, int64_t M);
+size_t forward_workspace_bytes(const FwdPlan &plan);
+// Number of tiles (workgroups) the search launches; must fit the grid.
+int64_t forward_tiles(const FwdPlan &plan);
 
-hipError_t launch_forward(const NNPlan &plan, hipStream_t stream);
+hipError_t launch_forward(const FwdPlan &plan, const FwdArgs &args, hipStream_t stream);
 
 hipError_t launch_reduce(int64_t B, int64_t N, int64_t M, const float *dist_xy,
                          const float *dist_yx, double w1, double w2, float *chamfer,

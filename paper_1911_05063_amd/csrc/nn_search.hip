@@ -1,31 +1,49 @@
 // Brute-force nearest-neighbour search in both directions for the batched
-// Chamfer distance (Kaolin Sec. 2.5: matching every point of one cloud to
+// Chamfer distance (Kaolin Sec. 2.5: every point of one cloud is matched to
 // the nearest point of the other), hand-written for gfx950.
 //
-// Design (FP32 VALU, not MFMA: the contraction is only 3 deep and the
-// difference-of-coordinates form is needed for accuracy on near points):
-//  * One wave per work item.  A work item is (direction, batch item, block of
-//    64*K queries, split of the targets).  Each lane keeps K queries in
-//    registers.
-//  * Targets are read with wave-uniform addresses, so they are fetched by the
-//    scalar unit into SGPRs and fed to the VALU as broadcast operands: no LDS
-//    traffic, no barriers, one s_load per few targets.
-//  * Per pair: 3 subtractions, one multiply and two FMAs in the fixed order
-//    fma(dz,dz, fma(dy,dy, dx*dx)), and half a v_min3 (two targets per min3).
-//  * Deferred argmin: the inner loop tracks only the running minimum.  After
-//    every sub-tile of kSubTile targets a lane notes the sub-tile if it
-//    lowered the minimum strictly; at the end the noted sub-tile is rescanned
-//    to find the lowest index whose distance equals the minimum.  The rescan
-//    recomputes the distance with the same instructions, so equality is exact.
-//  * Target splits (needed to fill 1024 SIMDs when there are few queries per
-//    item) are merged with a 64-bit atomicMin on (float bits << 32 | index),
-//    which orders by distance then index because distances are >= +0.
+// Fused symmetric search: every squared distance d(x_i, y_j) is evaluated
+// once and feeds both minima, x_i's nearest y (a row of the distance matrix)
+// and y_j's nearest x (a column).
+//
+//  * FP32 VALU, not MFMA: the contraction is only 3 deep, and the difference
+//    form fma(dz,dz, fma(dy,dy, dx*dx)) with d = x - y is needed for accuracy
+//    on near points (the |x|^2 + |y|^2 - 2x.y expansion cancels).
+//  * Tiles: a workgroup of kWaves waves owns a query group of
+//    kWaves*64*kQ x-points (kQ per lane, in registers, lane-major: lane l of
+//    the group holds x-points l*kQ .. l*kQ+kQ-1) and a block of TB y-points.
+//    The y-points are read with wave-uniform addresses, so the scalar unit
+//    loads them into SGPRs and the VALU takes them as broadcast operands.
+//  * Rows: per x-point a running minimum over the block, kept with v_min3
+//    (two targets per instruction).  The argmin is deferred: a lane only
+//    notes the batch of kBatch targets that last lowered its minimum strictly.
+//  * Columns: per lane and target, the minimum over the lane's kQ x-points;
+//    after each batch these partials are transposed through LDS so that each
+//    lane reduces one target's values (half a wave each), and the lowest
+//    lane holding the minimum is found.  The 4 waves combine through a 64-bit
+//    LDS atomicMin on (distance bits << 32 | lane), which orders by distance
+//    then lane because distances are >= +0.
+//  * Each tile writes one packed (distance, batch start) key per x-point and
+//    one (distance, lane) key per y-point to the workspace; a merge kernel
+//    takes the minimum key over tiles and recovers the exact lowest index by
+//    recomputing the kBatch candidate targets of a row or the kQ candidate
+//    x-points of a column with the same instructions, so equality is exact.
 #include "cd_internal.h"
 
 #include <algorithm>
 
 namespace cdk {
 namespace {
+
+constexpr int kQ = 8;               // x-points per lane
+constexpr int kWaves = 4;           // waves per workgroup
+constexpr int kThreads = kWaves * kWave;
+constexpr int kBatch = 32;          // targets per batch (row sub-tile, column batch)
+constexpr int kLdsRow = kWave + 4;  // padded LDS row (floats) of the column transpose
+constexpr int kMaxTB = 1024;        // targets per block at most (LDS column keys)
+constexpr int kMinTB = 256;         // targets per block at least
+constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (16 waves per CU on MI355X)
+constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
                                          float tz)
@@ -36,192 +54,289 @@ __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx,
     return __builtin_fmaf(dz, dz, __builtin_fmaf(dy, dy, dx * dx));
 }
 
-template <int K, int SUB>
-__global__ __launch_bounds__(kWave) void nn_search_kernel(NNPlan plan)
+// v_min3_f32 on values that are never NaN: no canonicalisation is needed.
+__device__ __forceinline__ float min3f(float a, float b, float c)
 {
-    static_assert(SUB % 2 == 0, "sub-tile holds target pairs");
-    const uint32_t item0 = blockIdx.x;
-    const bool second = item0 >= static_cast<uint32_t>(plan.d[0].items);
-    const float *P = second ? plan.d[1].P : plan.d[0].P;
-    const float *Q = second ? plan.d[1].Q : plan.d[0].Q;
-    float *dist = second ? plan.d[1].dist : plan.d[0].dist;
-    int32_t *idxo = second ? plan.d[1].idx : plan.d[0].idx;
-    unsigned long long *keys = second ? plan.d[1].keys : plan.d[0].keys;
-    const int NP = second ? plan.d[1].NP : plan.d[0].NP;
-    const int NQ = second ? plan.d[1].NQ : plan.d[0].NQ;
-    const uint32_t nqb = second ? plan.d[1].nqb : plan.d[0].nqb;
-    const uint32_t nsplit = second ? plan.d[1].nsplit : plan.d[0].nsplit;
-    const int chunk = second ? plan.d[1].chunk : plan.d[0].chunk;
-    const uint32_t item = second ? item0 - static_cast<uint32_t>(plan.d[0].items) : item0;
+    float r;
+    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
 
-    const uint32_t split = item % nsplit;
-    const uint32_t rest = item / nsplit;
-    const uint32_t qblk = rest % nqb;
-    const uint32_t b = rest / nqb;
+__device__ __forceinline__ float min2f(float a, float b)
+{
+    float r;
+    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 
-    const int lane = threadIdx.x;
-    const float *Pb = P + static_cast<int64_t>(b) * NP * 3;
-    const float *Qb = Q + static_cast<int64_t>(b) * NQ * 3;
-    const int q0 = static_cast<int>(qblk) * (kWave * K);
+__device__ __forceinline__ unsigned long long pack_key(float d, uint32_t low)
+{
+    return (static_cast<unsigned long long>(__float_as_uint(d)) << 32) | low;
+}
 
-    float qx[K], qy[K], qz[K], best[K];
-    int bsub[K];
-    const int t0 = static_cast<int>(split) * chunk;
-    const int t1 = t0 + min(chunk, NQ - t0);
+struct KernelArgs {
+    const float *X;
+    const float *Y;
+    unsigned long long *rowpart;  // [B, nTB, N]  (distance, batch start) per x-point and block
+    unsigned long long *colpart;  // [B, nQG, M]  (distance, x lane) per y-point and group
+    int32_t N, M, nQG, nTB, TB;
+    int32_t pad;
+    int64_t B;
+};
+
+// One batch of kBatch targets starting at j.  FULL: the whole batch lies in
+// [j, t1); otherwise the targets past t1 repeat target t1-1 (never chosen over
+// it: equal distances resolve to the lower index) and write no column key.
+template <bool FULL>
+__device__ __forceinline__ void search_batch(const float *__restrict__ Yb, int j, int t1,
+                                             const float (&qx)[kQ], const float (&qy)[kQ],
+                                             const float (&qz)[kQ], float (&best)[kQ],
+                                             int (&bsub)[kQ], float *lds, int lane,
+                                             unsigned long long *colkeys, int t0,
+                                             uint32_t lane0)
+{
+    float m[kQ];
+    float c[kBatch];
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const int64_t qc = min(static_cast<int64_t>(q0) + k * kWave + lane,
-                               static_cast<int64_t>(NP) - 1);
-        qx[k] = Pb[3 * qc + 0];
-        qy[k] = Pb[3 * qc + 1];
-        qz[k] = Pb[3 * qc + 2];
+    for (int jj = 0; jj < kBatch; jj += 2) {
+        int ja = j + jj, jb = j + jj + 1;
+        if (!FULL) {
+            ja = min(ja, t1 - 1);
+            jb = min(jb, t1 - 1);
+        }
+        const float ax = Yb[3 * ja + 0], ay = Yb[3 * ja + 1], az = Yb[3 * ja + 2];
+        const float bx = Yb[3 * jb + 0], by = Yb[3 * jb + 1], bz = Yb[3 * jb + 2];
+        float da[kQ], db[kQ];
+#pragma unroll
+        for (int k = 0; k < kQ; ++k) {
+            da[k] = sq_dist(qx[k], qy[k], qz[k], ax, ay, az);
+            db[k] = sq_dist(qx[k], qy[k], qz[k], bx, by, bz);
+            m[k] = (jj == 0) ? min2f(da[k], db[k]) : min3f(m[k], da[k], db[k]);
+        }
+        float ca = min3f(da[0], da[1], da[2]);
+        float cb = min3f(db[0], db[1], db[2]);
+#pragma unroll
+        for (int k = 3; k + 1 < kQ; k += 2) {
+            ca = min3f(ca, da[k], da[k + 1]);
+            cb = min3f(cb, db[k], db[k + 1]);
+        }
+        if ((kQ - 3) % 2 == 1) {
+            ca = min2f(ca, da[kQ - 1]);
+            cb = min2f(cb, db[kQ - 1]);
+        }
+        c[jj] = ca;
+        c[jj + 1] = cb;
+    }
+    // Rows: note the batch if it lowered the minimum strictly.
+#pragma unroll
+    for (int k = 0; k < kQ; ++k) {
+        const bool lower = m[k] < best[k];
+        best[k] = lower ? m[k] : best[k];
+        bsub[k] = lower ? j : bsub[k];
+    }
+
+    // Columns: transpose through LDS, lds[t * kLdsRow + lane] = c[t].  LDS
+    // operations of one wave execute in order, so no barrier is needed.
+#pragma unroll
+    for (int t = 0; t < kBatch; ++t) lds[t * kLdsRow + lane] = c[t];
+    __builtin_amdgcn_wave_barrier();
+    // Reducer lane r: target t = r % 32 over source lanes 32h .. 32h+31, h = r / 32.
+    const int t = lane & (kBatch - 1);
+    const int h = lane >> 5;
+    const float4 *row = reinterpret_cast<const float4 *>(lds + t * kLdsRow + h * 32);
+    float g[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float4 q = row[i];
+        g[i] = min2f(min3f(q.x, q.y, q.z), q.w);
+    }
+    const float mn = min2f(min3f(min3f(g[0], g[1], g[2]), g[3], g[4]), min3f(g[5], g[6], g[7]));
+    int fg = 7;
+#pragma unroll
+    for (int i = 6; i >= 0; --i) fg = (g[i] == mn) ? i : fg;
+    const float4 w = row[fg];
+    int fi = 3;
+    fi = (w.z == mn) ? 2 : fi;
+    fi = (w.y == mn) ? 1 : fi;
+    fi = (w.x == mn) ? 0 : fi;
+    const int first = 4 * fg + fi;  // lowest source lane (within the half) holding mn
+    __builtin_amdgcn_wave_barrier();
+    // Lanes r and r + 32 hold the two halves of target r: combine them.
+    const auto sm = __builtin_amdgcn_permlane32_swap(__float_as_uint(mn), __float_as_uint(mn),
+                                                     false, false);
+    const auto sf = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(first),
+                                                     static_cast<uint32_t>(first), false, false);
+    if (lane < kBatch) {
+        const float m0 = __uint_as_float(sm[0]), m1 = __uint_as_float(sm[1]);
+        const bool lo = m0 <= m1;
+        const uint32_t src = lo ? sf[0] : 32u + sf[1];
+        const int jt = j + lane;
+        if (FULL || jt < t1) atomicMin(colkeys + (jt - t0), pack_key(lo ? m0 : m1, lane0 + src));
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void search_kernel(KernelArgs a)
+{
+    __shared__ unsigned long long colkeys[kMaxTB];
+    __shared__ __attribute__((aligned(16))) float ldsbuf[kWaves][kBatch * kLdsRow];
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    // blockIdx.x = (b * nQG + qg) * nTB + tb
+    const uint32_t tb = blockIdx.x % static_cast<uint32_t>(a.nTB);
+    const uint32_t rest = blockIdx.x / static_cast<uint32_t>(a.nTB);
+    const uint32_t qg = rest % static_cast<uint32_t>(a.nQG);
+    const uint32_t b = rest / static_cast<uint32_t>(a.nQG);
+    const int t0 = static_cast<int>(tb) * a.TB;
+    const int t1 = t0 + min(a.TB, a.M - t0);
+    const float *Xb = a.X + static_cast<int64_t>(b) * a.N * 3;
+    const float *Yb = a.Y + static_cast<int64_t>(b) * a.M * 3;
+
+    for (int t = threadIdx.x; t < t1 - t0; t += kThreads) colkeys[t] = ~0ull;
+
+    const uint32_t lane0 = (qg * kWaves + wave) * kWave;  // first lane of this wave in the item
+    const int64_t xbase = static_cast<int64_t>(lane0 + lane) * kQ;
+    float qx[kQ], qy[kQ], qz[kQ], best[kQ];
+    int bsub[kQ];
+#pragma unroll
+    for (int k = 0; k < kQ; ++k) {
+        // x-points past N repeat x-point N-1, which has a lower index.
+        const int64_t qi = min(xbase + k, static_cast<int64_t>(a.N) - 1);
+        qx[k] = Xb[3 * qi + 0];
+        qy[k] = Xb[3 * qi + 1];
+        qz[k] = Xb[3 * qi + 2];
         best[k] = __builtin_inff();
         bsub[k] = t0;
     }
+    __syncthreads();
 
+    float *lds = ldsbuf[wave];
     int j = t0;
-    for (; t1 - j >= SUB; j += SUB) {
-        const float *T = Qb + 3 * static_cast<int64_t>(j);
-        float m[K];
-#pragma unroll
-        for (int jj = 0; jj < SUB; jj += 2) {
-            const float ax = T[3 * jj + 0], ay = T[3 * jj + 1], az = T[3 * jj + 2];
-            const float bx = T[3 * jj + 3], by = T[3 * jj + 4], bz = T[3 * jj + 5];
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const float da = sq_dist(qx[k], qy[k], qz[k], ax, ay, az);
-                const float db = sq_dist(qx[k], qy[k], qz[k], bx, by, bz);
-                m[k] = (jj == 0) ? fminf(da, db) : fminf(m[k], fminf(da, db));
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const bool lower = m[k] < best[k];
-            best[k] = lower ? m[k] : best[k];
-            bsub[k] = lower ? j : bsub[k];
-        }
-    }
-    if (j < t1) {  // ragged last sub-tile
-        float m[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) m[k] = __builtin_inff();
-        for (int jj = j; jj < t1; ++jj) {
-            const float *T = Qb + 3 * static_cast<int64_t>(jj);
-            const float tx = T[0], ty = T[1], tz = T[2];
-#pragma unroll
-            for (int k = 0; k < K; ++k) m[k] = fminf(m[k], sq_dist(qx[k], qy[k], qz[k], tx, ty, tz));
-        }
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const bool lower = m[k] < best[k];
-            best[k] = lower ? m[k] : best[k];
-            bsub[k] = lower ? j : bsub[k];
-        }
-    }
+    for (; t1 - j >= kBatch; j += kBatch)
+        search_batch<true>(Yb, j, t1, qx, qy, qz, best, bsub, lds, lane, colkeys, t0, lane0);
+    if (j < t1)
+        search_batch<false>(Yb, j, t1, qx, qy, qz, best, bsub, lds, lane, colkeys, t0, lane0);
 
-    // Recover the lowest index attaining the minimum inside the noted sub-tile.
+    unsigned long long *rp = a.rowpart + (static_cast<int64_t>(b) * a.nTB + tb) * a.N;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const int64_t qi = static_cast<int64_t>(q0) + k * kWave + lane;
-        if (qi < NP) {
-            const int jb = bsub[k];
-            const int je = jb + min(SUB, t1 - jb);
-            int found = -1;
-            for (int jj = je - 1; jj >= jb; --jj) {
-                const float *T = Qb + 3 * static_cast<int64_t>(jj);
-                const float d = sq_dist(qx[k], qy[k], qz[k], T[0], T[1], T[2]);
-                found = (d == best[k]) ? jj : found;
-            }
-            const int64_t o = static_cast<int64_t>(b) * NP + qi;
-            if (nsplit == 1) {
-                dist[o] = best[k];
-                idxo[o] = found;
-            } else {
-                const unsigned long long key =
-                    (static_cast<unsigned long long>(__float_as_uint(best[k])) << 32) |
-                    static_cast<uint32_t>(found);
-                atomicMin(keys + o, key);
-            }
-        }
-    }
+    for (int k = 0; k < kQ; ++k)
+        if (xbase + k < a.N) rp[xbase + k] = pack_key(best[k], static_cast<uint32_t>(bsub[k]));
+    __syncthreads();
+    unsigned long long *cp = a.colpart + (static_cast<int64_t>(b) * a.nQG + qg) * a.M;
+    for (int t = threadIdx.x; t < t1 - t0; t += kThreads) cp[t0 + t] = colkeys[t];
 }
 
-__global__ void fill_keys_kernel(unsigned long long *keys, int64_t n)
+// Thread per output point: threads [0, B*N) finish rows, the rest columns.
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
+                                                              int32_t *ixy, float *dyx,
+                                                              int32_t *iyx)
 {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i < n) keys[i] = ~0ull;
-}
-
-__global__ void unpack_keys_kernel(const unsigned long long *keys, float *dist, int32_t *idx,
-                                   int64_t n)
-{
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i < n) {
-        const unsigned long long key = keys[i];
-        dist[i] = __uint_as_float(static_cast<uint32_t>(key >> 32));
-        idx[i] = static_cast<int32_t>(static_cast<uint32_t>(key));
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * kMergeThreads + threadIdx.x;
+    const int64_t nx = a.B * a.N;
+    if (t >= nx + a.B * a.M) return;
+    if (t < nx) {
+        const int64_t b = t / a.N, i = t - b * a.N;
+        const unsigned long long *rp = a.rowpart + b * a.nTB * static_cast<int64_t>(a.N) + i;
+        unsigned long long key = ~0ull;
+#pragma unroll 8
+        for (int tb = 0; tb < a.nTB; ++tb) key = min(key, rp[static_cast<int64_t>(tb) * a.N]);
+        const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
+        int js = static_cast<int>(static_cast<uint32_t>(key));
+        js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
+        const int je = js + min(kBatch, a.M - js);
+        const float *x = a.X + 3 * t;
+        const float *Yb = a.Y + b * a.M * 3;
+        const float px = x[0], py = x[1], pz = x[2];
+        int found = -1;
+#pragma unroll 8
+        for (int jj = je - 1; jj >= js; --jj) {
+            const float d = sq_dist(px, py, pz, Yb[3 * jj], Yb[3 * jj + 1], Yb[3 * jj + 2]);
+            found = (d == val) ? jj : found;
+        }
+        dxy[t] = val;
+        ixy[t] = found;
+    } else {
+        const int64_t u = t - nx;
+        const int64_t b = u / a.M, jy = u - b * a.M;
+        const unsigned long long *cp = a.colpart + b * a.nQG * static_cast<int64_t>(a.M) + jy;
+        unsigned long long key = ~0ull;
+#pragma unroll 8
+        for (int q = 0; q < a.nQG; ++q) key = min(key, cp[static_cast<int64_t>(q) * a.M]);
+        const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
+        const int64_t i0 = static_cast<int64_t>(static_cast<uint32_t>(key)) * kQ;
+        const int64_t i1 = min(i0 + kQ, a.N);
+        const float *y = a.Y + 3 * u;
+        const float *Xb = a.X + b * a.N * 3;
+        const float px = y[0], py = y[1], pz = y[2];
+        int64_t found = -1;
+        for (int64_t ii = i1 - 1; ii >= i0; --ii) {
+            const float d = sq_dist(Xb[3 * ii], Xb[3 * ii + 1], Xb[3 * ii + 2], px, py, pz);
+            found = (d == val) ? ii : found;
+        }
+        dyx[u] = val;
+        iyx[u] = static_cast<int32_t>(found);
     }
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-}  // namespace
+struct WsOffsets {
+    size_t rowpart, colpart, total;
+};
 
-WsLayout workspace_layout(int64_t B, int64_t N, int64_t M)
+WsOffsets ws_offsets(const FwdPlan &p)
 {
     auto up = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
-    WsLayout w;
-    w.keys_xy = 0;
-    w.keys_yx = up(static_cast<size_t>(B * N) * 8);
-    w.total = w.keys_yx + up(static_cast<size_t>(B * M) * 8);
+    WsOffsets w;
+    w.rowpart = 0;
+    w.colpart = up(static_cast<size_t>(p.B) * p.nTB * p.N * 8);
+    w.total = w.colpart + up(static_cast<size_t>(p.B) * p.nQG * p.M * 8);
     return w;
 }
 
-void make_plan(NNPlan &plan, int64_t B, int64_t N, int64_t M, int cu_count)
+}  // namespace
+
+FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
 {
-    const int64_t qpb = static_cast<int64_t>(kWave) * kQueriesPerLane;
-    const int64_t NPs[2] = {N, M}, NQs[2] = {M, N};
-    // Equal-sized work items: about 4 waves per SIMD (4 SIMDs per CU), with
-    // at least 512 targets per split so the rescan stays a small fraction.
-    double work = 0.0;
-    for (int d = 0; d < 2; ++d) work += static_cast<double>(B) * ceil_div(NPs[d], qpb) * NQs[d];
-    const double target_items = static_cast<double>(std::max(cu_count, 1)) * 16.0;
-    int64_t chunk = static_cast<int64_t>(work / target_items) + 1;
-    chunk = std::max<int64_t>(chunk, 512);
-    for (int d = 0; d < 2; ++d) {
-        NNDir &D = plan.d[d];
-        D.NP = static_cast<int32_t>(NPs[d]);
-        D.NQ = static_cast<int32_t>(NQs[d]);
-        D.nqb = static_cast<int32_t>(ceil_div(NPs[d], qpb));
-        int64_t ns = ceil_div(NQs[d], chunk);
-        int64_t c = ceil_div(ceil_div(NQs[d], ns), kSubTile) * kSubTile;
-        ns = ceil_div(NQs[d], c);
-        D.nsplit = static_cast<int32_t>(ns);
-        D.chunk = static_cast<int32_t>(c);
-        D.pad = 0;
-        D.items = B * D.nqb * ns;
-    }
-    plan.B = B;
+    FwdPlan p;
+    p.B = B;
+    p.N = static_cast<int32_t>(N);
+    p.M = static_cast<int32_t>(M);
+    const int64_t per_group = static_cast<int64_t>(kThreads) * kQ;
+    p.nQG = static_cast<int32_t>(ceil_div(N, per_group));
+    // Split the targets until there are about kTargetTiles tiles, keeping
+    // blocks between kMinTB and kMaxTB targets and a multiple of kBatch.
+    const int64_t groups = std::max<int64_t>(1, B * p.nQG);
+    const int64_t want_blocks = ceil_div(kTargetTiles, groups);
+    int64_t TB = ceil_div(ceil_div(M, want_blocks), kBatch) * kBatch;
+    TB = std::min<int64_t>(std::max<int64_t>(TB, kMinTB), kMaxTB);
+    p.TB = static_cast<int32_t>(TB);
+    p.nTB = static_cast<int32_t>(ceil_div(M, TB));
+    return p;
 }
 
-hipError_t launch_forward(const NNPlan &plan, hipStream_t stream)
+size_t forward_workspace_bytes(const FwdPlan &p) { return ws_offsets(p).total; }
+
+int64_t forward_tiles(const FwdPlan &p) { return p.B * p.nQG * p.nTB; }
+
+hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream)
 {
-    const int64_t n[2] = {plan.B * plan.d[0].NP, plan.B * plan.d[1].NP};
-    for (int d = 0; d < 2; ++d) {
-        if (plan.d[d].nsplit > 1) {
-            fill_keys_kernel<<<static_cast<uint32_t>(ceil_div(n[d], 256)), 256, 0, stream>>>(
-                plan.d[d].keys, n[d]);
-        }
-    }
-    const int64_t items = plan.d[0].items + plan.d[1].items;
-    nn_search_kernel<kQueriesPerLane, kSubTile>
-        <<<static_cast<uint32_t>(items), kWave, 0, stream>>>(plan);
-    for (int d = 0; d < 2; ++d) {
-        if (plan.d[d].nsplit > 1) {
-            unpack_keys_kernel<<<static_cast<uint32_t>(ceil_div(n[d], 256)), 256, 0, stream>>>(
-                plan.d[d].keys, plan.d[d].dist, plan.d[d].idx, n[d]);
-        }
-    }
+    const WsOffsets w = ws_offsets(p);
+    KernelArgs a;
+    a.X = f.X;
+    a.Y = f.Y;
+    a.rowpart = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.rowpart);
+    a.colpart = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.colpart);
+    a.N = p.N;
+    a.M = p.M;
+    a.nQG = p.nQG;
+    a.nTB = p.nTB;
+    a.TB = p.TB;
+    a.pad = 0;
+    a.B = p.B;
+    search_kernel<<<static_cast<uint32_t>(forward_tiles(p)), kThreads, 0, stream>>>(a);
+    const int64_t total = p.B * (static_cast<int64_t>(p.N) + p.M);
+    merge_kernel<<<static_cast<uint32_t>(ceil_div(total, kMergeThreads)), kMergeThreads, 0,
+                   stream>>>(a, f.dist_xy, f.idx_xy, f.dist_yx, f.idx_yx);
     return hipGetLastError();
 }
 

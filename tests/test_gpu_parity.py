@@ -30,8 +30,9 @@ def _gpu():
 
 import paper_1911_05063_amd as cd  # noqa: E402
 
-# (kind, B, N, M, seed): ragged sizes that span several query blocks (512),
-# several sub-tiles (32) and target splits, plus the degenerate N=1 / M=1.
+# (kind, B, N, M, seed): ragged sizes that span several query groups (2048
+# x-points), target blocks (256-1024 y-points) and batches (32 y-points), plus
+# the degenerate N = 1 / M = 1.
 SMALL_CASES = [
     ("uniform", 1, 1024, 1024, 1),
     ("uniform", 2, 1000, 1500, 2),
@@ -144,6 +145,24 @@ def test_duplicates_across_splits_tie_to_lowest_index():
     ref = oracle.nn(X, Y, fused=True)
     gc.assert_nn_bitwise(g, ref, "dup")
     assert np.all(g[1] < 300)
+
+
+def test_column_duplicates_across_query_groups_tie_to_lowest_index():
+    # x-points repeated along the cloud so that copies of every y-point's
+    # nearest x fall in different lanes, waves, query groups and target
+    # blocks: the first copy must win in both directions.
+    X0, Y = synth.generate("grid_dup", 2, 700, 2500, 44)
+    X = np.concatenate([X0] * 9, axis=1)  # N = 6300: several query groups of 2048
+    g = gc.gpu_forward(X, Y)
+    gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), "xdup")
+    assert np.all(g[3] < 700)
+
+
+def test_many_tiles_ragged_both_ways():
+    # Neither N nor M a multiple of the query group (2048) or target block.
+    X, Y = synth.generate("uniform", 3, 4097, 5121, 45)
+    g = gc.gpu_forward(X, Y)
+    gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), "ragged")
 
 
 def test_empty_batch_is_noop():
