@@ -39,8 +39,9 @@ FLOPS_PER_PAIR = 9                # 3 sub + 3 mul + 2 add + 1 min per directed p
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps; the GPU clock ramps up during the first ~50 ms")
     ap.add_argument("--workload", type=int, default=3, help="workload number 1..5 (default 3)")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,

@@ -2,18 +2,24 @@
 // that supervises networks) for the neighbours the forward chose.
 //
 // d dist_xy[i] / d x_i = 2 (x_i - y_j) and d dist_xy[i] / d y_j = -2 (x_i - y_j)
-// for j = idx_xy[i]; symmetrically for dist_yx.  Two launches on the stream:
-//  1. own terms: every gX[i] / gY[j] is overwritten with its own direction's
-//     term (plain stores, so no clearing pass is needed);
-//  2. scatter terms: each point subtracts its term from its neighbour's
-//     gradient with a hardware float atomic add (global_atomic_add_f32).
-// Both are O(B (N + M)) and memory/atomic-latency bound.
+// for j = idx_xy[i]; symmetrically for dist_yx.  So
+//   gX[i] = 2 g_xy(i) (x_i - y_{idx_xy[i]}) - sum_{j: idx_yx[j] = i} 2 g_yx(j) (y_j - x_i)
+//   gY[j] = 2 g_yx(j) (y_j - x_{idx_yx[j]}) - sum_{i: idx_xy[i] = j} 2 g_xy(i) (x_i - y_j)
+//
+// One launch, no global atomics.  A workgroup owns a slice of kSlice points of
+// one cloud (the receiving side) of one item: it scans the other cloud's
+// neighbour indices, adds the scatter terms that land in its slice to LDS
+// accumulators (ds_add_f32), then writes own term + accumulated scatter once
+// per point.  Global float atomics on this chip are executed far from the CU
+// (about 20 G/s measured), LDS atomics next to it.  The order of the LDS
+// additions varies from run to run, so the last bits may too.
 #include "cd_internal.h"
 
 namespace cdk {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 1024;
+constexpr int kSlice = 4096;
 
 struct BwdArgs {
     const float *gxy;   // [B] (per item) or [B, N] (pointwise)
@@ -27,49 +33,71 @@ struct BwdArgs {
     int64_t B, N, M;
     float sxy, syx;     // per-item scale (w1/N, w2/M) when not pointwise
     int pointwise;
+    int nsx, nsy;       // slices of X and of Y per item
 };
 
-// Thread t < B*N handles x-point t (direction X->Y); the rest handle y-points.
-template <bool kScatter>
+// dL/d dist of point p (flat index) of cloud X (xdir) or Y, item b.
+__device__ __forceinline__ float weight(const BwdArgs &a, bool xdir, int64_t b, int64_t p)
+{
+    if (a.pointwise) return xdir ? a.gxy[p] : a.gyx[p];
+    return (xdir ? a.gxy[b] : a.gyx[b]) * (xdir ? a.sxy : a.syx);
+}
+
+// Workgroup (b, side, slice).  side 0 writes gX[b, slice], side 1 gY[b, slice].
 __global__ __launch_bounds__(kBlock) void backward_kernel(BwdArgs a)
 {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    const int64_t nx = a.B * a.N;
-    const int64_t total = nx + a.B * a.M;
-    if (t >= total) return;
-    const bool xdir = t < nx;
-    const int64_t p = xdir ? t : t - nx;                 // query point (flat)
-    const int64_t NP = xdir ? a.N : a.M;
-    const int64_t NQ = xdir ? a.M : a.N;
-    const int64_t b = p / NP;
-    const float *P = xdir ? a.X : a.Y;
-    const float *Q = xdir ? a.Y : a.X;
-    const int32_t nb = xdir ? a.idx_xy[p] : a.idx_yx[p];
-    if (nb < 0 || nb >= NQ) {  // not a neighbour index: the point contributes nothing
-        if (!kScatter) {
-            float *own = xdir ? a.gX : a.gY;
-            own[3 * p + 0] = 0.0f;
-            own[3 * p + 1] = 0.0f;
-            own[3 * p + 2] = 0.0f;
-        }
-        return;
+    __shared__ float acc[3][kSlice];
+    const int per_item = a.nsx + a.nsy;
+    const int64_t b = blockIdx.x / per_item;
+    const int r = blockIdx.x % per_item;
+    const bool xside = r < a.nsx;                 // receiving cloud is X
+    const int64_t s0 = static_cast<int64_t>(xside ? r : r - a.nsx) * kSlice;
+    const int64_t nrecv = xside ? a.N : a.M;      // points of the receiving cloud
+    const int64_t nsend = xside ? a.M : a.N;      // points of the other cloud
+    const int64_t s1 = min(s0 + kSlice, nrecv);
+    const float *R = (xside ? a.X : a.Y) + b * nrecv * 3;              // receiving, item b
+    const float *S = (xside ? a.Y : a.X) + b * nsend * 3;              // sending, item b
+    const int32_t *sidx = (xside ? a.idx_yx : a.idx_xy) + b * nsend;   // sender -> receiver
+    const int32_t *ridx = (xside ? a.idx_xy : a.idx_yx) + b * nrecv;   // receiver -> sender
+    float *out = (xside ? a.gX : a.gY) + b * nrecv * 3;
+
+    for (int t = threadIdx.x; t < kSlice; t += kBlock) {
+        acc[0][t] = 0.0f;
+        acc[1][t] = 0.0f;
+        acc[2][t] = 0.0f;
     }
-    const int64_t q = b * NQ + nb;  // neighbour (flat)
-    float g;
-    if (a.pointwise)
-        g = xdir ? a.gxy[p] : a.gyx[p];
-    else
-        g = (xdir ? a.gxy[b] : a.gyx[b]) * (xdir ? a.sxy : a.syx);
-    const float g2 = 2.0f * g;
-    float *own = xdir ? a.gX : a.gY;
-    float *nbr = xdir ? a.gY : a.gX;
+    __syncthreads();
+
+    // Scatter terms of senders whose neighbour lies in this slice:
+    // -2 g(s) (s - r) added to r.
+#pragma unroll 4
+    for (int64_t q = threadIdx.x; q < nsend; q += kBlock) {
+        const int64_t i = sidx[q];
+        if (i >= s0 && i < s1) {
+            const float g2 = 2.0f * weight(a, !xside, b, b * nsend + q);
+            const int64_t l = i - s0;
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
-        const float term = g2 * (P[3 * p + c] - Q[3 * q + c]);
-        if (kScatter)
-            unsafeAtomicAdd(nbr + 3 * q + c, -term);
-        else
-            own[3 * p + c] = term;
+            for (int c = 0; c < 3; ++c) {
+                const float term = g2 * (S[3 * q + c] - R[3 * i + c]);
+                atomicAdd(&acc[c][l], -term);
+            }
+        }
+    }
+    __syncthreads();
+
+    // Own term plus the accumulated scatter, written once per point.  A point
+    // whose neighbour index is out of range contributes nothing.
+    for (int64_t p = s0 + threadIdx.x; p < s1; p += kBlock) {
+        const int64_t l = p - s0;
+        const int32_t nb = ridx[p];
+        const bool ok = nb >= 0 && nb < nsend;
+        const float g2 = ok ? 2.0f * weight(a, xside, b, b * nrecv + p) : 0.0f;
+        const int64_t qn = ok ? nb : 0;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            const float own = ok ? g2 * (R[3 * p + c] - S[3 * qn + c]) : 0.0f;
+            out[3 * p + c] = own + acc[c][l];
+        }
     }
 }
 
@@ -80,11 +108,11 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
                            const float *X, const float *Y, const int32_t *idx_xy,
                            const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream)
 {
-    BwdArgs a{g_xy, g_yx, X, Y, idx_xy, idx_yx, gX, gY, B, N, M, sxy, syx, pointwise ? 1 : 0};
-    const int64_t total = B * (N + M);
-    const uint32_t grid = static_cast<uint32_t>((total + kBlock - 1) / kBlock);
-    backward_kernel<false><<<grid, kBlock, 0, stream>>>(a);
-    backward_kernel<true><<<grid, kBlock, 0, stream>>>(a);
+    BwdArgs a{g_xy, g_yx, X, Y, idx_xy, idx_yx, gX, gY, B, N, M, sxy, syx, pointwise ? 1 : 0,
+              static_cast<int>((N + kSlice - 1) / kSlice),
+              static_cast<int>((M + kSlice - 1) / kSlice)};
+    const int64_t grid = B * (a.nsx + a.nsy);
+    backward_kernel<<<static_cast<uint32_t>(grid), kBlock, 0, stream>>>(a);
     return hipGetLastError();
 }
 

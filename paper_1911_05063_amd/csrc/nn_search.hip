@@ -40,9 +40,9 @@ constexpr int kWaves = 4;           // waves per workgroup
 constexpr int kThreads = kWaves * kWave;
 constexpr int kBatch = 32;          // targets per batch (row sub-tile, column batch)
 constexpr int kLdsRow = kWave + 4;  // padded LDS row (floats) of the column transpose
-constexpr int kMaxTB = 1024;        // targets per block at most (LDS column keys)
+constexpr int kMaxTB = 512;         // targets per block at most (LDS column keys)
 constexpr int kMinTB = 256;         // targets per block at least
-constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (16 waves per CU on MI355X)
+constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (4 rounds of 4 per CU on MI355X)
 constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
@@ -175,7 +175,9 @@ __device__ __forceinline__ void search_batch(const float *__restrict__ Yb, int j
     }
 }
 
-__global__ __launch_bounds__(kThreads) void search_kernel(KernelArgs a)
+// At most 128 VGPRs (4 waves per SIMD) and 39 KB of LDS: 4 workgroups per CU.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
+void search_kernel(KernelArgs a)
 {
     __shared__ unsigned long long colkeys[kMaxTB];
     __shared__ __attribute__((aligned(16))) float ldsbuf[kWaves][kBatch * kLdsRow];
