@@ -18,8 +18,9 @@
 namespace cdk {
 namespace {
 
-constexpr int kBlock = 1024;
-constexpr int kSlice = 4096;
+constexpr int kBlock = 512;
+constexpr int kSlice = 2048;
+constexpr int kUnroll = 8;
 
 struct BwdArgs {
     const float *gxy;   // [B] (per item) or [B, N] (pointwise)
@@ -69,17 +70,39 @@ __global__ __launch_bounds__(kBlock) void backward_kernel(BwdArgs a)
     __syncthreads();
 
     // Scatter terms of senders whose neighbour lies in this slice:
-    // -2 g(s) (s - r) added to r.
-#pragma unroll 4
-    for (int64_t q = threadIdx.x; q < nsend; q += kBlock) {
-        const int64_t i = sidx[q];
-        if (i >= s0 && i < s1) {
-            const float g2 = 2.0f * weight(a, !xside, b, b * nsend + q);
-            const int64_t l = i - s0;
+    // -2 g(s) (s - r) added to r.  kUnroll senders per thread per round, with
+    // every load issued before the first wait (out-of-slice lanes read a
+    // clamped, valid address and add nothing).
+    const bool spw = a.pointwise != 0;
+    const float g2s_item = spw ? 0.0f : 2.0f * weight(a, !xside, b, 0);
+    const float *gsend = (xside ? a.gyx : a.gxy) + (spw ? b * nsend : 0);  // [B, n] only if pointwise
+    for (int64_t base = 0; base < nsend; base += static_cast<int64_t>(kBlock) * kUnroll) {
+        int64_t qs[kUnroll], is[kUnroll];
+        bool in[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t q = base + static_cast<int64_t>(u) * kBlock + threadIdx.x;
+            qs[u] = min(q, nsend - 1);
+            const int64_t i = sidx[qs[u]];
+            in[u] = q < nsend && i >= s0 && i < s1;
+            is[u] = in[u] ? i : s0;
+        }
+        float sv[kUnroll][3], rv[kUnroll][3], g2[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
             for (int c = 0; c < 3; ++c) {
-                const float term = g2 * (S[3 * q + c] - R[3 * i + c]);
-                atomicAdd(&acc[c][l], -term);
+                sv[u][c] = S[3 * qs[u] + c];
+                rv[u][c] = R[3 * is[u] + c];
+            }
+            g2[u] = spw ? 2.0f * gsend[qs[u]] : g2s_item;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            if (in[u]) {
+                const int64_t l = is[u] - s0;
+#pragma unroll
+                for (int c = 0; c < 3; ++c) atomicAdd(&acc[c][l], -(g2[u] * (sv[u][c] - rv[u][c])));
             }
         }
     }
@@ -87,15 +110,18 @@ __global__ __launch_bounds__(kBlock) void backward_kernel(BwdArgs a)
 
     // Own term plus the accumulated scatter, written once per point.  A point
     // whose neighbour index is out of range contributes nothing.
+    const float g2r_item = spw ? 0.0f : 2.0f * weight(a, xside, b, 0);
+    const float *grecv = (xside ? a.gxy : a.gyx) + (spw ? b * nrecv : 0);
+#pragma unroll 4
     for (int64_t p = s0 + threadIdx.x; p < s1; p += kBlock) {
         const int64_t l = p - s0;
         const int32_t nb = ridx[p];
         const bool ok = nb >= 0 && nb < nsend;
-        const float g2 = ok ? 2.0f * weight(a, xside, b, b * nrecv + p) : 0.0f;
         const int64_t qn = ok ? nb : 0;
+        const float g2 = ok ? (spw ? 2.0f * grecv[p] : g2r_item) : 0.0f;
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-            const float own = ok ? g2 * (R[3 * p + c] - S[3 * qn + c]) : 0.0f;
+            const float own = g2 * (R[3 * p + c] - S[3 * qn + c]);
             out[3 * p + c] = own + acc[c][l];
         }
     }

@@ -196,13 +196,15 @@ void search_kernel(KernelArgs a)
     for (int t = threadIdx.x; t < t1 - t0; t += kThreads) colkeys[t] = ~0ull;
 
     const uint32_t lane0 = (qg * kWaves + wave) * kWave;  // first lane of this wave in the item
-    const int64_t xbase = static_cast<int64_t>(lane0 + lane) * kQ;
+    // x-point index of this lane's first x-point; below N + kThreads*kQ < 2^32.
+    const uint32_t xbase = (lane0 + static_cast<uint32_t>(lane)) * kQ;
+    const uint32_t nx = static_cast<uint32_t>(a.N);
     float qx[kQ], qy[kQ], qz[kQ], best[kQ];
     int bsub[kQ];
 #pragma unroll
     for (int k = 0; k < kQ; ++k) {
         // x-points past N repeat x-point N-1, which has a lower index.
-        const int64_t qi = min(xbase + k, static_cast<int64_t>(a.N) - 1);
+        const int64_t qi = min(xbase + k, nx - 1);
         qx[k] = Xb[3 * qi + 0];
         qy[k] = Xb[3 * qi + 1];
         qz[k] = Xb[3 * qi + 2];
@@ -221,7 +223,7 @@ void search_kernel(KernelArgs a)
     unsigned long long *rp = a.rowpart + (static_cast<int64_t>(b) * a.nTB + tb) * a.N;
 #pragma unroll
     for (int k = 0; k < kQ; ++k)
-        if (xbase + k < a.N) rp[xbase + k] = pack_key(best[k], static_cast<uint32_t>(bsub[k]));
+        if (xbase + k < nx) rp[xbase + k] = pack_key(best[k], static_cast<uint32_t>(bsub[k]));
     __syncthreads();
     unsigned long long *cp = a.colpart + (static_cast<int64_t>(b) * a.nQG + qg) * a.M;
     for (int t = threadIdx.x; t < t1 - t0; t += kThreads) cp[t0 + t] = colkeys[t];

@@ -47,9 +47,9 @@ __global__ __launch_bounds__(kBlock) void chamfer_reduce_kernel(int64_t N, int64
     const float *a = dxy + b * N;
     const float *c = dyx + b * M;
     double sx = 0.0, sy = 0.0;
-#pragma unroll 4
+#pragma unroll 16
     for (int64_t i = threadIdx.x; i < N; i += kBlock) sx += static_cast<double>(a[i]);
-#pragma unroll 4
+#pragma unroll 16
     for (int64_t j = threadIdx.x; j < M; j += kBlock) sy += static_cast<double>(c[j]);
     sx = block_sum(sx, scratch);
     sy = block_sum(sy, scratch);
@@ -67,9 +67,9 @@ __global__ __launch_bounds__(kBlock) void fscore_kernel(int64_t N, int64_t M, co
     const float *a = dxy + b * N;
     const float *c = dyx + b * M;
     unsigned long long cp = 0, cr = 0;
-#pragma unroll 4
+#pragma unroll 16
     for (int64_t i = threadIdx.x; i < N; i += kBlock) cp += (a[i] < thr) ? 1u : 0u;
-#pragma unroll 4
+#pragma unroll 16
     for (int64_t j = threadIdx.x; j < M; j += kBlock) cr += (c[j] < thr) ? 1u : 0u;
     cp = block_sum(cp, scratch);
     cr = block_sum(cr, scratch);
