@@ -3,8 +3,8 @@
 
 A step is one pass of the whole path over one batch of synthetic clouds that
 are already resident in HBM: nearest neighbours both ways (cd_forward), the
-Chamfer reduction (cd_reduce), the F-score at every threshold of the workload
-(cd_fscore) and the backward to both clouds (cd_backward).  The default
+Chamfer reduction and the F-score at every threshold of the workload (one
+cd_metrics call) and the backward to both clouds (cd_backward).  The default
 workload is B=16, N=M=16384 points sampled on random 200-triangle meshes with
 F-score at tau = 0.005, 0.01, 0.02.
 
@@ -34,6 +34,7 @@ if ROOT not in sys.path:
 METRIC = "Chamfer fwd+bwd pair-evals/sec and ms/call at B=16, N=M=16384; % FP32 VALU peak"
 PEAK_FP32_TFLOPS = 157.3          # MI355X FP32 vector, 256 CU x 2.4 GHz x 256 flop/clk
 FLOPS_PER_PAIR = 9                # 3 sub + 3 mul + 2 add + 1 min per directed pair-eval
+FORWARD_SOURCES = ("paper_1911_05063_amd/csrc/nn_search.hip",)  # kernels of cd_forward
 
 
 def parse_args():
@@ -46,7 +47,28 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, fill then copy an MIB-MiB device buffer once: "
+                         "reference kernels of known size for HBM-counter calibration")
     return ap.parse_args()
+
+
+def traffic_record(kernel_sources):
+    """HBM bytes per cd_forward from the committed counter summary, or None when
+    the kernel sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_mesh_b16_n16384.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for src in kernel_sources:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if rec.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return rec
 
 
 class Step:
@@ -71,7 +93,9 @@ class Step:
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         self.chamfer = torch.empty(B, dtype=f32, device=dev)
         self.taus = list(taus)
-        self.fs = [[torch.empty(B, dtype=f32, device=dev) for _ in range(3)] for _ in self.taus]
+        self.fs = [torch.empty((len(self.taus), B), dtype=f32, device=dev) for _ in range(3)]
+        self.tau_arr = (ctypes.c_float * len(self.taus))(*self.taus)
+        self.tau_ptr = ctypes.cast(self.tau_arr, ctypes.c_void_p)
         self.grad_out = torch.ones(B, dtype=f32, device=dev)
         self.gX = torch.empty_like(X)
         self.gY = torch.empty_like(Y)
@@ -80,8 +104,8 @@ class Step:
         P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
         self.p = {k: P(v) for k, v in dict(X=X, Y=Y, dxy=self.dxy, ixy=self.ixy, dyx=self.dyx,
                                            iyx=self.iyx, ws=self.ws, ch=self.chamfer,
-                                           go=self.grad_out, gX=self.gX, gY=self.gY).items()}
-        self.pf = [[P(t) for t in trio] for trio in self.fs]
+                                           go=self.grad_out, gX=self.gX, gY=self.gY,
+                                           f=self.fs[0], pr=self.fs[1], rc=self.fs[2]).items()}
 
     def _ok(self, st, what):
         if st != 0:
@@ -94,12 +118,11 @@ class Step:
                                      p["dyx"], p["iyx"], p["ws"], self.ws_bytes, self.s), "cd_forward")
 
     def reduce_fscore(self):
+        """Chamfer and F-score at every tau: one cd_metrics launch."""
         p = self.p
-        self._ok(self.lib.cd_reduce(self.B, self.N, self.M, p["dxy"], p["dyx"], 1.0, 1.0, p["ch"],
-                                    self.s), "cd_reduce")
-        for tau, (f, pr, rc) in zip(self.taus, self.pf):
-            self._ok(self.lib.cd_fscore(self.B, self.N, self.M, p["dxy"], p["dyx"], float(tau), f,
-                                        pr, rc, self.s), "cd_fscore")
+        self._ok(self.lib.cd_metrics(self.B, self.N, self.M, p["dxy"], p["dyx"], 1.0, 1.0,
+                                     self.tau_ptr, len(self.taus), p["ch"], p["f"], p["pr"],
+                                     p["rc"], self.s), "cd_metrics")
 
     def backward(self):
         p = self.p
@@ -179,6 +202,16 @@ def main():
     red = [e[1].elapsed_time(e[2]) for e in evs]
     bwd = [e[2].elapsed_time(e[3]) for e in evs]
 
+    if args.calib_copy > 0:
+        n = args.calib_copy * (1 << 20) // 4
+        src = torch.empty(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     B, N, M = w.B, w.N, w.M
     pairs = 2.0 * B * N * M
     ms_per_step = total_ms / args.steps
@@ -208,8 +241,12 @@ def main():
         "roofline": {"bound": "alu", "kernel": "cd_forward (search_kernel + merge_kernel)",
                      "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+                     "algorithmic_bytes": 12.0 * B * (N + M) + 8.0 * B * (N + M),
                      "work_per_launch": f"{FLOPS_PER_PAIR} flop x {pairs:.4g} directed pair-evals"},
     }
+    tr = traffic_record(FORWARD_SOURCES) if args.workload == 3 else None
+    if tr is not None:
+        out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
     if not args.no_cpu_baseline:
         items = args.cpu_items if args.cpu_items > 0 else B
         print(f"[bench] CPU oracle baseline on {items} item(s)", file=sys.stderr, flush=True)

@@ -113,6 +113,19 @@ cd_status cd_fscore(int64_t B, int64_t N, int64_t M,
                     float *f, float *precision, float *recall, hipStream_t stream);
 
 /*
+ * Chamfer reduction and F-score at several thresholds in one pass over the
+ * distances (the two calls above, fused; results are bitwise identical to
+ * them).  taus [ntau] is HOST memory (read during the call); chamfer [B],
+ * f / precision / recall [ntau, B] are device memory (precision and recall
+ * may be NULL; chamfer and f may not).  1 <= ntau <= 16, every tau >= 0 and
+ * not NaN, else CD_ERR_INVALID_ARG.
+ */
+cd_status cd_metrics(int64_t B, int64_t N, int64_t M,
+                     const float *dist_xy, const float *dist_yx, float w1, float w2,
+                     const float *taus, int ntau, float *chamfer,
+                     float *f, float *precision, float *recall, hipStream_t stream);
+
+/*
  * Backward of sum_b grad_out[b] * chamfer[b] (the Chamfer loss used to
  * supervise networks, Sec. 2.5), for the neighbours cd_forward chose:
  *   gX[b,i] = 2 g_xy (x_i - y_{idx_xy[i]}) - sum_{j: idx_yx[j]=i} 2 g_yx (y_j - x_i)

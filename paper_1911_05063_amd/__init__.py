@@ -10,6 +10,7 @@ Functions (names follow the C ABI):
   nn_distance(X, Y)                 -> dist_xy, idx_xy, dist_yx, idx_yx
   chamfer_reduce(dist_xy, dist_yx)  -> chamfer [B]
   f_score(dist_xy, dist_yx, tau)    -> f, precision, recall  [B] each
+  metrics(dist_xy, dist_yx, taus)   -> chamfer [B], f / precision / recall [ntau, B]
   chamfer_backward(...)             -> gX, gY
   chamfer_distance(X, Y, w1, w2)    -> chamfer [B], differentiable (autograd)
 """
@@ -23,7 +24,7 @@ import torch
 
 __all__ = [
     "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "chamfer_reduce",
-    "f_score", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
+    "f_score", "metrics", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
     "ChamferDistance", "forward_step",
 ]
 
@@ -60,6 +61,8 @@ def library() -> ctypes.CDLL:
     lib.cd_reduce.argtypes = [i64, i64, i64, vp, vp, f32, f32, vp, vp]
     lib.cd_fscore.restype = st
     lib.cd_fscore.argtypes = [i64, i64, i64, vp, vp, f32, vp, vp, vp, vp]
+    lib.cd_metrics.restype = st
+    lib.cd_metrics.argtypes = [i64, i64, i64, vp, vp, f32, f32, vp, ctypes.c_int, vp, vp, vp, vp, vp]
     lib.cd_backward.restype = st
     lib.cd_backward.argtypes = [i64, i64, i64, vp, f32, f32, vp, vp, vp, vp, vp, vp, vp]
     lib.cd_backward_pointwise.restype = st
@@ -151,6 +154,25 @@ def f_score(dist_xy: torch.Tensor, dist_yx: torch.Tensor, tau: float):
         _check(library().cd_fscore(B, N, M, _ptr(dxy), _ptr(dyx), float(tau), _ptr(f), _ptr(p),
                                    _ptr(r), ctypes.c_void_p(_stream(dxy.device))), "cd_fscore")
     return f, p, r
+
+
+def metrics(dist_xy: torch.Tensor, dist_yx: torch.Tensor, taus, w1: float = 1.0,
+            w2: float = 1.0):
+    """Chamfer [B] and F-score at each tau ([ntau, B] f, precision, recall) in one launch."""
+    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
+    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
+    taus = [float(t) for t in taus]
+    ntau = len(taus)
+    tau_arr = (ctypes.c_float * max(ntau, 1))(*taus)
+    ch = torch.empty(B, dtype=torch.float32, device=dxy.device)
+    f, p, r = (torch.empty((ntau, B), dtype=torch.float32, device=dxy.device) for _ in range(3))
+    with torch.cuda.device(dxy.device):
+        _check(library().cd_metrics(B, N, M, _ptr(dxy), _ptr(dyx), float(w1), float(w2),
+                                    ctypes.cast(tau_arr, ctypes.c_void_p), ntau, _ptr(ch), _ptr(f),
+                                    _ptr(p), _ptr(r), ctypes.c_void_p(_stream(dxy.device))),
+               "cd_metrics")
+    return ch, f, p, r
 
 
 def chamfer_backward(grad_out: torch.Tensor, X: torch.Tensor, Y: torch.Tensor,

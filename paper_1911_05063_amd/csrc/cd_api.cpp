@@ -45,6 +45,16 @@ cd_status check_shape(int64_t B, int64_t N, int64_t M)
 
 bool aligned256(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 
+// A float32 squared distance d satisfies d < tau^2 (exact in double for a
+// float tau) iff d < thr, where thr is the smallest float32 >= tau^2.
+float threshold_of(float tau)
+{
+    const double t2 = static_cast<double>(tau) * static_cast<double>(tau);
+    float thr = static_cast<float>(t2);
+    if (static_cast<double>(thr) < t2) thr = std::nextafter(thr, INFINITY);
+    return thr;
+}
+
 }  // namespace
 
 extern "C" {
@@ -115,14 +125,31 @@ cd_status cd_fscore(int64_t B, int64_t N, int64_t M, const float *dist_xy, const
     if (std::isnan(tau) || tau < 0.0f) return invalid("tau must be >= 0 and not NaN");
     if (B == 0) return CD_OK;
     if (!dist_xy || !dist_yx || !f) return invalid("NULL array pointer");
-    // A float32 squared distance d satisfies d < tau^2 (exact in double) iff
-    // d < thr, where thr is the smallest float32 >= tau^2.
-    const double t2 = static_cast<double>(tau) * static_cast<double>(tau);
-    float thr = static_cast<float>(t2);
-    if (static_cast<double>(thr) < t2) thr = std::nextafter(thr, INFINITY);
+    const float thr = threshold_of(tau);
     const hipError_t e =
         cdk::launch_fscore(B, N, M, dist_xy, dist_yx, thr, f, precision, recall, stream);
     if (e != hipSuccess) return hip_failed(e, "cd_fscore launch");
+    return CD_OK;
+}
+
+cd_status cd_metrics(int64_t B, int64_t N, int64_t M, const float *dist_xy, const float *dist_yx,
+                     float w1, float w2, const float *taus, int ntau, float *chamfer, float *f,
+                     float *precision, float *recall, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (!taus || ntau < 1 || ntau > cdk::kMaxTaus) return invalid("need 1 <= ntau <= 16 and taus");
+    float thr[cdk::kMaxTaus];
+    for (int t = 0; t < ntau; ++t) {
+        if (std::isnan(taus[t]) || taus[t] < 0.0f) return invalid("tau must be >= 0 and not NaN");
+        thr[t] = threshold_of(taus[t]);
+    }
+    if (B == 0) return CD_OK;
+    if (!dist_xy || !dist_yx || !chamfer || !f) return invalid("NULL array pointer");
+    const hipError_t e = cdk::launch_metrics(B, N, M, dist_xy, dist_yx, static_cast<double>(w1),
+                                             static_cast<double>(w2), thr, ntau, chamfer, f,
+                                             precision, recall, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_metrics launch");
     return CD_OK;
 }
 

@@ -47,6 +47,15 @@ hipError_t launch_fscore(int64_t B, int64_t N, int64_t M, const float *dist_xy,
                          const float *dist_yx, float thr, float *f, float *precision,
                          float *recall, hipStream_t stream);
 
+constexpr int kMaxTaus = 16;
+
+// Chamfer (w1, w2 given) and F-score counts for ntau thresholds (thr[] are the
+// float32 thresholds compared against the squared distances) in one launch.
+hipError_t launch_metrics(int64_t B, int64_t N, int64_t M, const float *dist_xy,
+                          const float *dist_yx, double w1, double w2, const float *thr,
+                          int ntau, float *chamfer, float *f, float *precision, float *recall,
+                          hipStream_t stream);
+
 // g_xy/g_yx per point when `pointwise`, else per item (grad_out) scaled by
 // sxy = w1/N and syx = w2/M.
 hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,

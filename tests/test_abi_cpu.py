@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_header_declares_the_path():
     names = declared_functions()
-    for n in ("cd_forward", "cd_reduce", "cd_fscore", "cd_backward", "cd_backward_pointwise",
+    for n in ("cd_forward", "cd_reduce", "cd_fscore", "cd_metrics", "cd_backward", "cd_backward_pointwise",
               "cd_workspace_bytes", "cd_status_string", "cd_last_error", "cd_version"):
         assert n in names
 
@@ -121,6 +121,23 @@ def test_reduce_fscore_backward_reject_bad_args(lib):
         a = [FAKE] * 8
         a[k] = None
         assert lib.cd_backward_pointwise(1, 3, 3, *a, None) == CD_ERR_INVALID_ARG
+
+
+def test_metrics_rejects_bad_args(lib):
+    taus = (ctypes.c_float * 17)(*([0.1] * 17))
+    tp = ctypes.cast(taus, ctypes.c_void_p)
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, tp, 0, FAKE, FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, tp, 17, FAKE, FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, None, 2, FAKE, FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    bad = (ctypes.c_float * 2)(0.1, float("nan"))
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, ctypes.cast(bad, ctypes.c_void_p), 2, FAKE, FAKE,
+                          None, None, None) == CD_ERR_INVALID_ARG
+    neg = (ctypes.c_float * 1)(-1.0)
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, ctypes.cast(neg, ctypes.c_void_p), 1, FAKE, FAKE,
+                          None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, tp, 3, None, FAKE, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_metrics(1, 3, 3, FAKE, FAKE, 1.0, 1.0, tp, 3, FAKE, None, None, None, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_metrics(0, 3, 3, None, None, 1.0, 1.0, tp, 3, None, None, None, None, None) == CD_OK
 
 
 def test_binding_refuses_cpu_tensors():

@@ -84,6 +84,22 @@ def test_reduce_fscore_backward_match_oracle(case):
     gc.assert_grad(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx), go, w1, w2)
 
 
+@pytest.mark.parametrize("case", SMALL_CASES[:6] + [("uniform", 1, 1, 1, 9)], ids=_case_id)
+def test_metrics_equals_reduce_and_fscore(case):
+    kind, B, N, M, seed = case
+    X, Y = synth.generate(kind, B, N, M, seed)
+    dxy, _, dyx, _ = cd.nn_distance(gc.to_gpu(X), gc.to_gpu(Y))
+    taus = [0.005, 0.01, 0.02, 0.05, 0.1, 1.5]
+    ch, f, p, r = (gc.to_np(t) for t in cd.metrics(dxy, dyx, taus, 0.75, 1.25))
+    assert np.array_equal(ch, gc.to_np(cd.chamfer_reduce(dxy, dyx, 0.75, 1.25)))
+    dxy_n, dyx_n = gc.to_np(dxy), gc.to_np(dyx)
+    gc.assert_chamfer(ch, dxy_n, dyx_n, 0.75, 1.25)
+    for t, tau in enumerate(taus):
+        f1, p1, r1 = (gc.to_np(v) for v in cd.f_score(dxy, dyx, tau))
+        assert np.array_equal(f[t], f1) and np.array_equal(p[t], p1) and np.array_equal(r[t], r1)
+        gc.assert_fscore(f[t], p[t], r[t], dxy_n, dyx_n, tau)
+
+
 def test_backward_pointwise_matches_oracle():
     X, Y = synth.generate("grid_dup", 2, 900, 1100, 21)
     Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
@@ -205,6 +221,7 @@ def test_full_size_workload(k):
     go = np.linspace(1.0, 2.0, w.B).astype(np.float32)
     gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
     fs = {t: cd.f_score(dxy, dyx, t) for t in w.taus}
+    mch, mf, mp, mr = cd.metrics(dxy, dyx, w.taus)
     torch.cuda.synchronize()
     dxy_n, ixy_n, dyx_n, iyx_n = (gc.to_np(t) for t in (dxy, ixy, dyx, iyx))
     rng = np.random.default_rng(1000 + k)
@@ -216,8 +233,10 @@ def test_full_size_workload(k):
         assert np.array_equal(idx[rows[:, 0], rows[:, 1]], ri)
     assert ixy_n.min() >= 0 and ixy_n.max() < w.M and iyx_n.min() >= 0 and iyx_n.max() < w.N
     gc.assert_chamfer(gc.to_np(ch), dxy_n, dyx_n)
-    for t, (f, p, r) in fs.items():
+    assert np.array_equal(gc.to_np(mch), gc.to_np(ch))
+    for ti, (t, (f, p, r)) in enumerate(fs.items()):
         gc.assert_fscore(gc.to_np(f), gc.to_np(p), gc.to_np(r), dxy_n, dyx_n, t)
+        assert np.array_equal(gc.to_np(mf)[ti], gc.to_np(f))
     gXn, gYn = gc.to_np(gX), gc.to_np(gY)
     gc.assert_grad(gXn, gYn, X, Y, ixy_n, iyx_n, go)
     gc.gradient_identities(gXn, gYn, X, Y, go, oracle.chamfer(dxy_n, dyx_n))
