@@ -47,26 +47,79 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
+    ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="read two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; each with "
+                         "--calib-copy 256), write profiles/traffic_mesh_b16_n16384.json, exit")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="after the timed steps, fill then copy an MIB-MiB device buffer once: "
                          "reference kernels of known size for HBM-counter calibration")
     return ap.parse_args()
 
 
+def _sources_sha256(kernel_sources):
+    import hashlib
+    h = hashlib.sha256()
+    for src in kernel_sources:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def ingest_pmc(fetch_dir, write_dir, calib_mib=256):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of cd_forward's kernels, each
+    scaled by what the counter reads for the calibration copy of calib_mib MiB."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    def averages(d):
+        paths = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not paths:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        acc = defaultdict(list)
+        with open(paths[0]) as f:
+            for row in csv.DictReader(f):
+                acc[row["Kernel_Name"]].append(float(row["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in acc.items()}
+
+    def pick(avg, key):
+        hits = [v for k, v in avg.items() if key in k]
+        if len(hits) != 1:
+            raise SystemExit(f"expected one kernel matching {key!r}, found {len(hits)}")
+        return hits[0]
+
+    fa, wa = averages(fetch_dir), averages(write_dir)
+    ref_kib = calib_mib * 1024.0
+    fs = ref_kib / pick(fa, "copyBuffer")
+    ws = ref_kib / pick(wa, "copyBuffer")
+    raw = {k: {"FETCH_SIZE": pick(fa, k), "WRITE_SIZE": pick(wa, k)}
+           for k in ("search_kernel", "merge_kernel")}
+    fetch = sum(r["FETCH_SIZE"] for r in raw.values()) * fs * 1024.0
+    write = sum(r["WRITE_SIZE"] for r in raw.values()) * ws * 1024.0
+    rec = {"kernel_source_sha256": _sources_sha256(FORWARD_SOURCES),
+           "workload": "mesh_b16_n16384 (B=16, N=M=16384)",
+           "launch": "cd_forward = search_kernel + merge_kernel",
+           "hbm_bytes_per_launch": round(fetch + write),
+           "fetch_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
+           "per_kernel_kib_raw": {k: {c: round(v, 1) for c, v in r.items()} for k, r in raw.items()},
+           "calibration": {"reference": f"__amd_rocclr_copyBuffer of {calib_mib} MiB",
+                           "fetch_scale": round(fs, 4), "write_scale": round(ws, 4)},
+           "algorithmic_bytes_per_launch": 20 * 16 * (16384 + 16384)}
+    out = os.path.join(ROOT, "profiles", "traffic_mesh_b16_n16384.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def traffic_record(kernel_sources):
     """HBM bytes per cd_forward from the committed counter summary, or None when
     the kernel sources changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "traffic_mesh_b16_n16384.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    h = hashlib.sha256()
-    for src in kernel_sources:
-        with open(os.path.join(ROOT, src), "rb") as f:
-            h.update(f.read())
-    if rec.get("kernel_source_sha256") != h.hexdigest():
+    if rec.get("kernel_source_sha256") != _sources_sha256(kernel_sources):
         return None
     return rec
 
@@ -151,6 +204,9 @@ def time_cpu_oracle(X, Y, taus, items):
 
 def main():
     args = parse_args()
+    if args.ingest_pmc:
+        ingest_pmc(*args.ingest_pmc)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the batch items are independent: shard them across GPUs).", file=sys.stderr)

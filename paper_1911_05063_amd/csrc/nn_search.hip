@@ -104,8 +104,10 @@ __device__ __forceinline__ void search_batch(const float *__restrict__ Yb, int j
             ja = min(ja, t1 - 1);
             jb = min(jb, t1 - 1);
         }
-        const float ax = Yb[3 * ja + 0], ay = Yb[3 * ja + 1], az = Yb[3 * ja + 2];
-        const float bx = Yb[3 * jb + 0], by = Yb[3 * jb + 1], bz = Yb[3 * jb + 2];
+        const float *ta = Yb + 3 * static_cast<int64_t>(ja);  // 64-bit: 3*M may pass 2^31
+        const float *tb = Yb + 3 * static_cast<int64_t>(jb);
+        const float ax = ta[0], ay = ta[1], az = ta[2];
+        const float bx = tb[0], by = tb[1], bz = tb[2];
         float da[kQ], db[kQ];
 #pragma unroll
         for (int k = 0; k < kQ; ++k) {
@@ -253,7 +255,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         int found = -1;
 #pragma unroll 8
         for (int jj = je - 1; jj >= js; --jj) {
-            const float d = sq_dist(px, py, pz, Yb[3 * jj], Yb[3 * jj + 1], Yb[3 * jj + 2]);
+            const float *ty = Yb + 3 * static_cast<int64_t>(jj);
+            const float d = sq_dist(px, py, pz, ty[0], ty[1], ty[2]);
             found = (d == val) ? jj : found;
         }
         dxy[t] = val;

@@ -181,6 +181,45 @@ def test_many_tiles_ragged_both_ways():
     gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), "ragged")
 
 
+@pytest.mark.parametrize("B,N,M", [(1, 1, 200000), (1, 300000, 1), (2, 70000, 3),
+                                   (1, 5, 100000), (600, 40, 50)],
+                         ids=lambda v: str(v))
+def test_extreme_shapes(B, N, M):
+    # One x-point against many targets, many x-points against one target,
+    # and many small items: every tiling extreme of the planner.
+    X, Y = synth.generate("uniform", B, N, M, 46 + N % 7)
+    g = gc.gpu_forward(X, Y)
+    gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), f"B{B}-N{N}-M{M}")
+
+
+def test_target_cloud_past_2pow30_points():
+    # M = 2^30 + 3 y-points (3*M floats > 2^31): 64-bit addressing at the
+    # largest size that fits comfortably.  Built on the GPU; closed form: the
+    # bulk of Y sits at (100,100,100), three planted points lie near x-points.
+    M = (1 << 30) + 3
+    dev = "cuda:0"
+    X = torch.tensor([[[0, 0, 0], [4, 0, 0], [0, 4, 0], [0, 0, 4], [-4, 0, 0]]],
+                     dtype=torch.float32, device=dev)
+    Y = torch.full((1, M, 3), 100.0, dtype=torch.float32, device=dev)
+    far, mid = M - 1, 800_000_123
+    Y[0, far] = torch.tensor([0.25, 0.0, 0.0], device=dev)
+    Y[0, mid] = torch.tensor([4.0, 0.5, 0.0], device=dev)
+    Y[0, 2] = torch.tensor([0.0, 4.0, 0.125], device=dev)
+    dxy, ixy, dyx, iyx = cd.nn_distance(X, Y)
+    torch.cuda.synchronize()
+    assert dxy.cpu().tolist() == [[0.0625, 0.25, 0.015625, 16.0625, 18.0625]]
+    assert ixy.cpu().tolist() == [[far, mid, 2, far, far]]
+    # Bulk points: (96,100,100)-type offsets to x1, x2, x3 tie at 29216; lowest index 1.
+    special = torch.tensor([2, mid, far], device=dev)
+    want_d = torch.full((M,), 29216.0, device=dev)
+    want_i = torch.ones((M,), dtype=torch.int32, device=dev)
+    want_d[special] = torch.tensor([0.015625, 0.25, 0.0625], device=dev)
+    want_i[special] = torch.tensor([2, 1, 0], dtype=torch.int32, device=dev)
+    assert torch.equal(dyx[0], want_d) and torch.equal(iyx[0], want_i)
+    del X, Y, dxy, ixy, dyx, iyx, want_d, want_i
+    torch.cuda.empty_cache()
+
+
 def test_empty_batch_is_noop():
     X = torch.empty((0, 5, 3), dtype=torch.float32, device="cuda:0")
     Y = torch.empty((0, 7, 3), dtype=torch.float32, device="cuda:0")
