@@ -12,6 +12,9 @@ Two independent implementations live here:
 * ``check64`` (NumPy, float64): brute force used to pin the C oracle -- it
   classifies near-ties, supplies the finite-difference gradient reference and
   brackets the F-score against threshold rounding.
+* ``mesh_oracle.c``: differentiable surface sampling of triangle meshes
+  (Kaolin Sec. 2.1, reparameterization trick): area-weighted face choice,
+  reparameterised points and their backward to the vertices, in double.
 
 Every function follows Kaolin Sec. 2.5 (Chamfer distance for point clouds,
 defined through its citation of Fan et al.) under the readings listed in the
@@ -29,6 +32,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cd_oracle.c")
+_MESH_SRC = os.path.join(_HERE, "mesh_oracle.c")
 LIB_PATH = os.path.join(_HERE, "libcd_oracle.so")
 
 _lib = None
@@ -37,7 +41,7 @@ _lib = None
 def build(verbose: bool = False) -> str:
     """Compile the C oracle (gcc, no FP contraction, OpenMP) into oracle/libcd_oracle.so."""
     cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
-           "-fPIC", "-shared", _SRC, "-o", LIB_PATH + ".tmp", "-lm"]
+           "-fPIC", "-shared", _SRC, _MESH_SRC, "-o", LIB_PATH + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
@@ -60,6 +64,11 @@ def _load():
                                   f64p, f64p]
     lib.oracle_backward_pointwise.argtypes = [i64, i64, i64, f64p, f64p, f32p, f32p, f32p, f32p,
                                               f64p, f64p, f64p, f64p, f32p, f32p]
+    vp = ctypes.c_void_p
+    lib.oracle_face_areas.argtypes = [i64, i64, i64, vp, vp, vp]
+    lib.oracle_sample_faces.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp]
+    lib.oracle_sample_points.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp, vp]
+    lib.oracle_sample_backward.argtypes = [i64, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -166,3 +175,68 @@ def forward_all(X, Y, taus=(0.01,), w1: float = 1.0, w2: float = 1.0, fused: boo
     cd = chamfer(dxy, dyx, w1, w2)
     fs = {float(t): fscore(dxy, dyx, t) for t in taus}
     return dict(dist_xy=dxy, idx_xy=ixy, dist_yx=dyx, idx_yx=iyx, chamfer=cd, fscore=fs)
+
+
+# ---------------------------------------------------------------- mesh sampling
+# Kaolin Sec. 2.1: differentiable surface sampling (reparameterization trick).
+
+def _mesh(V, F):
+    V = np.ascontiguousarray(V, np.float32)
+    F = np.ascontiguousarray(F, np.int32)
+    if V.ndim != 3 or V.shape[2] != 3 or F.ndim != 3 or F.shape[2] != 3 or F.shape[0] != V.shape[0]:
+        raise ValueError("expected V [B, nv, 3] float and F [B, nf, 3] int")
+    if F.size and (F.min() < 0 or F.max() >= V.shape[1]):
+        raise ValueError("face index out of range")
+    return V, F
+
+
+def face_areas(V, F) -> np.ndarray:
+    """Area of every face [B, nf] in double."""
+    V, F = _mesh(V, F)
+    out = np.empty(F.shape[:2], np.float64)
+    _load().oracle_face_areas(V.shape[0], V.shape[1], F.shape[1], _ptr(V), _ptr(F), _ptr(out))
+    return out
+
+
+def sample_faces(V, F, u) -> np.ndarray:
+    """Area-weighted face choice for uniforms u [B, S]: first f with u*total < cdf_f."""
+    V, F = _mesh(V, F)
+    u = np.ascontiguousarray(u, np.float32)
+    B, S = u.shape
+    scratch = np.empty(F.shape[:2], np.float64)
+    out = np.empty((B, S), np.int32)
+    _load().oracle_sample_faces(B, V.shape[1], F.shape[1], _ptr(V), _ptr(F), S, _ptr(u),
+                                _ptr(scratch), _ptr(out))
+    return out
+
+
+def sample_points(V, F, fidx, r1, r2) -> np.ndarray:
+    """Reparameterised samples P [B, S, 3] (float64) on the chosen faces."""
+    V, F = _mesh(V, F)
+    fidx = np.ascontiguousarray(fidx, np.int32)
+    r1 = np.ascontiguousarray(r1, np.float32)
+    r2 = np.ascontiguousarray(r2, np.float32)
+    B, S = fidx.shape
+    if fidx.size and (fidx.min() < 0 or fidx.max() >= F.shape[1]):
+        raise ValueError("face choice out of range")
+    out = np.empty((B, S, 3), np.float64)
+    _load().oracle_sample_points(B, V.shape[1], F.shape[1], _ptr(V), _ptr(F), S, _ptr(fidx),
+                                 _ptr(r1), _ptr(r2), _ptr(out))
+    return out
+
+
+def sample_backward(V, F, fidx, r1, r2, gP):
+    """(gV [B, nv, 3], sV, nV): gradient of sum(gP * P) w.r.t. the vertices,
+    per-component absolute sums and per-vertex contribution counts."""
+    V, F = _mesh(V, F)
+    fidx = np.ascontiguousarray(fidx, np.int32)
+    r1 = np.ascontiguousarray(r1, np.float32)
+    r2 = np.ascontiguousarray(r2, np.float32)
+    gP = np.ascontiguousarray(gP, np.float64)
+    B, S = fidx.shape
+    gV = np.empty(V.shape, np.float64)
+    sV = np.empty(V.shape, np.float64)
+    nV = np.empty(V.shape[:2], np.int32)
+    _load().oracle_sample_backward(B, V.shape[1], F.shape[1], _ptr(F), S, _ptr(fidx), _ptr(r1),
+                                   _ptr(r2), _ptr(gP), _ptr(gV), _ptr(sV), _ptr(nV))
+    return gV, sV, nV

@@ -32,7 +32,8 @@ from typing import Dict, Tuple
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "generate", "workload", "lattice_pair"]
+__all__ = ["Workload", "WORKLOADS", "generate", "workload", "lattice_pair", "triangle_soup",
+           "grid_mesh", "uniforms"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -206,3 +207,43 @@ def lattice_pair(B: int, dims: Tuple[int, int, int], h: float, shift, seed: int)
     if not (np.array_equal(Xf.astype(np.float64), X) and np.array_equal(Yf.astype(np.float64), Y)):
         raise ValueError("lattice is not exactly representable in float32")
     return Xf, Yf, perm
+
+
+def triangle_soup(B: int, n_tri: int, seed: int, sigma: float = 0.3):
+    """Independent triangles: V [B, 3*n_tri, 3] with vertices N(0, sigma^2), F [B, n_tri, 3]
+    (face t uses vertices 3t, 3t+1, 3t+2) -- the meshes of the mesh workload."""
+    rng = np.random.default_rng(seed)
+    V = rng.normal(0.0, sigma, (B, 3 * n_tri, 3))
+    F = np.broadcast_to(np.arange(3 * n_tri, dtype=np.int32).reshape(n_tri, 3), (B, n_tri, 3))
+    return _f32(V), np.ascontiguousarray(F)
+
+
+def grid_mesh(B: int, n: int, seed: int, amp: float = 0.1):
+    """A triangulated n x n height field per item (vertices shared by up to six
+    faces): V [B, n*n, 3] on [-1,1]^2 with heights amp * N(0,1), F [B, 2(n-1)^2, 3]."""
+    rng = np.random.default_rng(seed)
+    gx, gy = np.meshgrid(np.linspace(-1.0, 1.0, n), np.linspace(-1.0, 1.0, n), indexing="ij")
+    V = np.empty((B, n * n, 3))
+    for b in range(B):
+        V[b, :, 0] = gx.ravel()
+        V[b, :, 1] = gy.ravel()
+        V[b, :, 2] = amp * rng.standard_normal(n * n)
+    i, j = np.meshgrid(np.arange(n - 1), np.arange(n - 1), indexing="ij")
+    v00 = (i * n + j).ravel()
+    v10 = ((i + 1) * n + j).ravel()
+    v01 = (i * n + j + 1).ravel()
+    v11 = ((i + 1) * n + j + 1).ravel()
+    faces = np.concatenate([np.stack([v00, v10, v11], 1), np.stack([v00, v11, v01], 1)])
+    F = np.broadcast_to(faces.astype(np.int32), (B,) + faces.shape)
+    return _f32(V), np.ascontiguousarray(F)
+
+
+def uniforms(B: int, S: int, seed: int, count: int = 3):
+    """`count` arrays of float32 uniforms in [0, 1), shape [B, S] each (the random
+    numbers a sampler draws, drawn here and passed in)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        u = rng.random((B, S)).astype(np.float32)
+        out.append(np.minimum(u, np.float32(np.nextafter(np.float32(1), np.float32(0)))))
+    return tuple(out)
