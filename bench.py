@@ -44,6 +44,10 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=100,
                     help="untimed steps; the GPU clock ramps up during the first ~50 ms")
     ap.add_argument("--workload", type=int, default=3, help="workload number 1..5 (default 3)")
+    ap.add_argument("--path", choices=("chamfer", "mesh"), default="chamfer",
+                    help="chamfer: the Chamfer step on the workload (default); mesh: the mesh "
+                         "reconstruction loss step (surface sampling -> Chamfer -> vertex "
+                         "gradients) on 16 meshes of 200 triangles, 16384 samples each")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
@@ -202,8 +206,93 @@ def time_cpu_oracle(X, Y, taus, items):
                        f"{len(taus)} thresholds and backward, OpenMP over queries")}
 
 
+def mesh_step_bench(args):
+    """The mesh reconstruction loss step (Sec. 2.1 sampling feeding the Sec. 2.5
+    Chamfer loss): choose faces, sample points, Chamfer + F-score against a
+    target cloud, Chamfer backward, sampling backward to the vertices."""
+    import numpy as np
+    import torch
+    import paper_1911_05063_amd as cd
+    import synth
+
+    B, T, S, M = 16, 200, 16384, 16384
+    V_np, F_np = synth.triangle_soup(B, T, 3)
+    _, Y_np = synth.generate("mesh", B, 1, M, 30)
+    u_np, r1_np, r2_np = synth.uniforms(B, S, 31)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = lambda a: torch.from_numpy(np.array(a, copy=True)).to(dev)  # noqa: E731
+    V, F, Y, u, r1, r2 = (g(a) for a in (V_np, F_np, Y_np, u_np, r1_np, r2_np))
+    lib = cd.library()
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    mws = torch.empty(int(lib.cd_mesh_workspace_bytes(B, 3 * T, T, S)), dtype=torch.uint8, device=dev)
+    fidx = torch.empty((B, S), dtype=torch.int32, device=dev)
+    X = torch.empty((B, S, 3), dtype=torch.float32, device=dev)
+    step = Step(X, Y, (0.005, 0.01, 0.02))
+    gV = torch.empty_like(V)
+
+    def ok(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what}: {lib.cd_last_error().decode()}")
+
+    def one(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ok(lib.cd_mesh_sample_faces(B, 3 * T, T, P(V), P(F), S, P(u), P(fidx), P(mws),
+                                    mws.numel(), st), "faces")
+        ok(lib.cd_mesh_sample_points(B, 3 * T, T, P(V), P(F), S, P(fidx), P(r1), P(r2), P(X), st),
+           "points")
+        if ev is not None:
+            ev[1].record(stream)
+        step.forward()
+        step.reduce_fscore()
+        step.backward()
+        if ev is not None:
+            ev[2].record(stream)
+        ok(lib.cd_mesh_sample_backward(B, 3 * T, T, P(F), S, P(fidx), P(r1), P(r2), P(step.gX),
+                                       P(gV), P(mws), mws.numel(), st), "sample backward")
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(args.steps):
+        one(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    samp = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
+    cham = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
+    sbwd = statistics.mean(e[2].elapsed_time(e[3]) for e in evs)
+    pairs = 2.0 * B * S * M
+    out = {"metric": "mesh reconstruction loss step pair-evals/sec (sampling + Chamfer fwd+bwd + "
+                     "sampling bwd)",
+           "value": pairs / (ms * 1e-3), "unit": "pair-evals/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic",
+           "config": {"workload": "mesh_sampling_b16_t200_s16384", "B": B, "triangles": T,
+                      "samples": S, "M": M, "taus": [0.005, 0.01, 0.02]},
+           "ms_per_call": {"sample_faces+points": samp, "chamfer_fwd_metrics_bwd": cham,
+                           "sample_backward": sbwd},
+           "pct_fp32_valu_peak": 100.0 * FLOPS_PER_PAIR * pairs / (ms * 1e-3) / (PEAK_FP32_TFLOPS * 1e12)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse_args()
+    if args.path == "mesh":
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        mesh_step_bench(args)
+        return
     if args.ingest_pmc:
         ingest_pmc(*args.ingest_pmc)
         return

@@ -153,6 +153,66 @@ cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M,
                                 const int32_t *idx_xy, const int32_t *idx_yx,
                                 float *gX, float *gY, hipStream_t stream);
 
+/*
+ * Differentiable surface sampling of triangle meshes (Kaolin Sec. 2.1: mesh to
+ * point-cloud conversion with the reparameterization trick), the step that
+ * turns a predicted mesh into the point cloud the Chamfer loss compares.
+ * Per item b: vertices V [B, nv, 3] float32, faces F [B, nf, 3] int32 (vertex
+ * indices of item b), S samples.  The random numbers are inputs: u, r1, r2
+ * [B, S] float32 in [0, 1).  A face with a vertex index outside [0, nv) has
+ * area 0; a sample whose face index is outside [0, nf) gets a NaN point and no
+ * gradient.  Checks (else CD_ERR_INVALID_ARG, nothing launched): B >= 0,
+ * nv >= 1, nf >= 1, S >= 0, nv, nf, S < 2^31, B * S <= 2^31,
+ * B * ceil(nv / 2048) <= 2^23.  B == 0 is a no-op; with S == 0 the forward
+ * calls are no-ops and the backward writes gV = 0.
+ */
+
+/*
+ * Device workspace bytes cd_mesh_sample_faces and cd_mesh_sample_backward need
+ * for these sizes (the larger of the per-item cumulative face areas, 8 B nf,
+ * and the backward's per-chunk vertex partial sums, at most about 48 MiB);
+ * 0 for sizes the checks below reject.  One buffer serves both calls.
+ */
+size_t cd_mesh_workspace_bytes(int64_t B, int64_t nv, int64_t nf, int64_t S);
+
+/*
+ * Area-weighted face choice: fidx[b, s] = the first face f whose cumulative
+ * area (faces 0..f) exceeds u[b, s] * total area.  Areas |(b-a) x (c-a)| / 2
+ * are evaluated in float32, rounded to multiples of 2^-k (k chosen per item so
+ * the total stays below 2^62, i.e. a resolution of about 2^-61 nf times the
+ * largest area) and cumulated exactly in int64, so a face of zero area (or
+ * with an out-of-range vertex) is never chosen.  A mesh of total area 0 gives
+ * -1.  The choice is bitwise reproducible.
+ * ws: cd_mesh_workspace_bytes(B, nv, nf, S) bytes, 256-byte aligned
+ * (CD_ERR_WORKSPACE if smaller).
+ */
+cd_status cd_mesh_sample_faces(int64_t B, int64_t nv, int64_t nf, const float *V,
+                               const int32_t *F, int64_t S, const float *u, int32_t *fidx,
+                               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Reparameterised samples: P[b, s] = (1 - sqrt(r1)) a + sqrt(r1) (1 - r2) b
+ * + sqrt(r1) r2 c for the face fidx[b, s] = (a, b, c).  P [B, S, 3] float32.
+ */
+cd_status cd_mesh_sample_points(int64_t B, int64_t nv, int64_t nf, const float *V,
+                                const int32_t *F, int64_t S, const int32_t *fidx,
+                                const float *r1, const float *r2, float *P, hipStream_t stream);
+
+/*
+ * Backward of the samples: gV [B, nv, 3] = d(sum gP . P) / dV, i.e. each
+ * sample adds its barycentric weight times gP[b, s] to each of its face's
+ * three vertices.  gV is fully overwritten (vertices no sample touches get 0).
+ * Each contribution w * gP is rounded from float32 to a 64-bit fixed-point
+ * integer (grid 2^-k, k from the largest |gP| of a chunk of samples, about
+ * 2^-61 / chunk length relative to it), summed exactly, and chunks are added
+ * in double in a fixed order: the result is bitwise reproducible run to run.
+ * ws: as for cd_mesh_sample_faces.
+ */
+cd_status cd_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const int32_t *F,
+                                  int64_t S, const int32_t *fidx, const float *r1,
+                                  const float *r2, const float *gP, float *gV, void *ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

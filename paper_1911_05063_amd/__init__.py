@@ -13,6 +13,9 @@ Functions (names follow the C ABI):
   metrics(dist_xy, dist_yx, taus)   -> chamfer [B], f / precision / recall [ntau, B]
   chamfer_backward(...)             -> gX, gY
   chamfer_distance(X, Y, w1, w2)    -> chamfer [B], differentiable (autograd)
+  mesh_sample_faces / mesh_sample_points / mesh_sample_backward
+                                    -> differentiable mesh surface sampling (Sec. 2.1)
+  sample_points(V, F, S)            -> P [B, S, 3], differentiable in V (autograd)
 """
 from __future__ import annotations
 
@@ -25,7 +28,8 @@ import torch
 __all__ = [
     "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "chamfer_reduce",
     "f_score", "metrics", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
-    "ChamferDistance", "forward_step",
+    "ChamferDistance", "forward_step", "mesh_sample_faces", "mesh_sample_points",
+    "mesh_sample_backward", "MeshSample", "sample_points",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcd_hip.so")
@@ -65,6 +69,15 @@ def library() -> ctypes.CDLL:
     lib.cd_metrics.argtypes = [i64, i64, i64, vp, vp, f32, f32, vp, ctypes.c_int, vp, vp, vp, vp, vp]
     lib.cd_backward.restype = st
     lib.cd_backward.argtypes = [i64, i64, i64, vp, f32, f32, vp, vp, vp, vp, vp, vp, vp]
+    lib.cd_mesh_workspace_bytes.restype = ctypes.c_size_t
+    lib.cd_mesh_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.cd_mesh_sample_faces.restype = st
+    lib.cd_mesh_sample_faces.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.cd_mesh_sample_points.restype = st
+    lib.cd_mesh_sample_points.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp]
+    lib.cd_mesh_sample_backward.restype = st
+    lib.cd_mesh_sample_backward.argtypes = [i64, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp,
+                                            ctypes.c_size_t, vp]
     lib.cd_backward_pointwise.restype = st
     lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     _lib = lib
@@ -243,3 +256,94 @@ def forward_step(X, Y, taus=(0.01,), w1: float = 1.0, w2: float = 1.0, workspace
     fs = {float(t): f_score(dist_xy, dist_yx, t) for t in taus}
     return dict(dist_xy=dist_xy, idx_xy=idx_xy, dist_yx=dist_yx, idx_yx=idx_yx, chamfer=cd,
                 fscore=fs)
+
+
+# ---------------------------------------------------------------- mesh sampling
+
+def _mesh(V: torch.Tensor, F: torch.Tensor):
+    V = _device_tensor(V, "V", torch.float32)
+    F = _device_tensor(F, "F", torch.int32)
+    if V.dim() != 3 or V.shape[2] != 3 or F.dim() != 3 or F.shape[2] != 3 or F.shape[0] != V.shape[0]:
+        raise ValueError("expected V [B, nv, 3] float32 and F [B, nf, 3] int32")
+    if V.device != F.device:
+        raise ValueError("V and F must share a device")
+    return V, F
+
+
+def _mesh_ws(B, nv, nf, S, device):
+    need = int(library().cd_mesh_workspace_bytes(B, nv, nf, S))
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+
+def mesh_sample_faces(V: torch.Tensor, F: torch.Tensor, u: torch.Tensor) -> torch.Tensor:
+    """Area-weighted face choice fidx [B, S] for uniforms u [B, S] (Sec. 2.1)."""
+    V, F = _mesh(V, F)
+    u = _device_tensor(u, "u", torch.float32)
+    B, nv, nf, S = V.shape[0], V.shape[1], F.shape[1], u.shape[1]
+    lib = library()
+    ws = _mesh_ws(B, nv, nf, S, V.device)
+    fidx = torch.empty((B, S), dtype=torch.int32, device=V.device)
+    with torch.cuda.device(V.device):
+        _check(lib.cd_mesh_sample_faces(B, nv, nf, _ptr(V), _ptr(F), S, _ptr(u), _ptr(fidx),
+                                        _ptr(ws), ws.numel(), ctypes.c_void_p(_stream(V.device))),
+               "cd_mesh_sample_faces")
+    return fidx
+
+
+def mesh_sample_points(V, F, fidx, r1, r2) -> torch.Tensor:
+    """Reparameterised surface samples P [B, S, 3] on the faces fidx."""
+    V, F = _mesh(V, F)
+    fidx = _device_tensor(fidx, "fidx", torch.int32)
+    r1 = _device_tensor(r1, "r1", torch.float32)
+    r2 = _device_tensor(r2, "r2", torch.float32)
+    B, nv, nf, S = V.shape[0], V.shape[1], F.shape[1], fidx.shape[1]
+    P = torch.empty((B, S, 3), dtype=torch.float32, device=V.device)
+    with torch.cuda.device(V.device):
+        _check(library().cd_mesh_sample_points(B, nv, nf, _ptr(V), _ptr(F), S, _ptr(fidx), _ptr(r1),
+                                               _ptr(r2), _ptr(P), ctypes.c_void_p(_stream(V.device))),
+               "cd_mesh_sample_points")
+    return P
+
+
+def mesh_sample_backward(nv: int, F, fidx, r1, r2, gP) -> torch.Tensor:
+    """gV [B, nv, 3]: gradient of sum(gP * P) with respect to the vertices."""
+    F = _device_tensor(F, "F", torch.int32)
+    fidx = _device_tensor(fidx, "fidx", torch.int32)
+    r1 = _device_tensor(r1, "r1", torch.float32)
+    r2 = _device_tensor(r2, "r2", torch.float32)
+    gP = _device_tensor(gP, "gP", torch.float32)
+    B, nf, S = F.shape[0], F.shape[1], fidx.shape[1]
+    gV = torch.empty((B, int(nv), 3), dtype=torch.float32, device=F.device)
+    ws = _mesh_ws(B, int(nv), nf, S, F.device)
+    with torch.cuda.device(F.device):
+        _check(library().cd_mesh_sample_backward(B, int(nv), nf, _ptr(F), S, _ptr(fidx), _ptr(r1),
+                                                 _ptr(r2), _ptr(gP), _ptr(gV), _ptr(ws), ws.numel(),
+                                                 ctypes.c_void_p(_stream(F.device))),
+               "cd_mesh_sample_backward")
+    return gV
+
+
+class MeshSample(torch.autograd.Function):
+    """P = sample(V) for fixed faces and uniforms, differentiable in V."""
+
+    @staticmethod
+    def forward(ctx, V, F, fidx, r1, r2):
+        ctx.save_for_backward(F, fidx, r1, r2)
+        ctx.nv = V.shape[1]
+        return mesh_sample_points(V, F, fidx, r1, r2)
+
+    @staticmethod
+    def backward(ctx, gP):
+        F, fidx, r1, r2 = ctx.saved_tensors
+        return mesh_sample_backward(ctx.nv, F, fidx, r1, r2, gP.float()), None, None, None, None
+
+
+def sample_points(V: torch.Tensor, F: torch.Tensor, num_samples: int, generator=None):
+    """Differentiable surface sampling of B meshes: returns (P [B, S, 3], fidx).
+    The uniforms are drawn with torch on the device (input generation); the
+    face choice and the samples are computed by the library's kernels."""
+    B = V.shape[0]
+    u, r1, r2 = (torch.rand((B, int(num_samples)), device=V.device, generator=generator)
+                 for _ in range(3))
+    fidx = mesh_sample_faces(V.detach(), F, u)
+    return MeshSample.apply(V, F, fidx, r1, r2), fidx

@@ -186,4 +186,82 @@ cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M, const float *g_
     return CD_OK;
 }
 
+static cd_status check_mesh(int64_t B, int64_t nv, int64_t nf, int64_t S)
+{
+    if (B < 0) return invalid("B < 0");
+    if (nv < 1 || nf < 1) return invalid("a mesh needs nv >= 1 and nf >= 1");
+    if (S < 0) return invalid("S < 0");
+    if (nv > kMaxPoints || nf > kMaxPoints || S > kMaxPoints) return invalid("nv, nf or S >= 2^31");
+    // Per-sample kernels launch B * S threads and the backward B * ceil(nv / 2048)
+    // workgroups (times a bounded number of sample chunks).
+    if (B > 0 && (B * S > (int64_t(1) << 31) || B * ((nv + 2047) / 2048) > (int64_t(1) << 23)))
+        return invalid("B * S > 2^31 or B * ceil(nv / 2048) > 2^23");
+    return CD_OK;
+}
+
+size_t cd_mesh_workspace_bytes(int64_t B, int64_t nv, int64_t nf, int64_t S)
+{
+    if (check_mesh(B, nv, nf, S) != CD_OK) return 0;
+    return (cdk::mesh_workspace_bytes(B, nv, nf, S) + 255) & ~static_cast<size_t>(255);
+}
+
+static cd_status check_mesh_ws(int64_t B, int64_t nv, int64_t nf, int64_t S, const void *ws,
+                               size_t ws_bytes)
+{
+    const size_t need = cd_mesh_workspace_bytes(B, nv, nf, S);
+    if (need == 0) return CD_OK;
+    if (!ws || ws_bytes < need) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
+        return CD_ERR_WORKSPACE;
+    }
+    if (!aligned256(ws)) return invalid("workspace not 256-byte aligned");
+    return CD_OK;
+}
+
+cd_status cd_mesh_sample_faces(int64_t B, int64_t nv, int64_t nf, const float *V, const int32_t *F,
+                               int64_t S, const float *u, int32_t *fidx, void *ws, size_t ws_bytes,
+                               hipStream_t stream)
+{
+    cd_status s = check_mesh(B, nv, nf, S);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!V || !F || (S > 0 && (!u || !fidx))) return invalid("NULL array pointer");
+    s = check_mesh_ws(B, nv, nf, S, ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e = cdk::launch_mesh_choose_faces(B, nv, nf, V, F, S, u, fidx, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_mesh_sample_faces launch");
+    return CD_OK;
+}
+
+cd_status cd_mesh_sample_points(int64_t B, int64_t nv, int64_t nf, const float *V,
+                                const int32_t *F, int64_t S, const int32_t *fidx, const float *r1,
+                                const float *r2, float *P, hipStream_t stream)
+{
+    cd_status s = check_mesh(B, nv, nf, S);
+    if (s != CD_OK) return s;
+    if (B == 0 || S == 0) return CD_OK;
+    if (!V || !F || !fidx || !r1 || !r2 || !P) return invalid("NULL array pointer");
+    const hipError_t e = cdk::launch_mesh_sample_points(B, nv, nf, V, F, S, fidx, r1, r2, P, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_mesh_sample_points launch");
+    return CD_OK;
+}
+
+cd_status cd_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const int32_t *F, int64_t S,
+                                  const int32_t *fidx, const float *r1, const float *r2,
+                                  const float *gP, float *gV, void *ws, size_t ws_bytes,
+                                  hipStream_t stream)
+{
+    cd_status s = check_mesh(B, nv, nf, S);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!F || !gV || (S > 0 && (!fidx || !r1 || !r2 || !gP))) return invalid("NULL array pointer");
+    s = check_mesh_ws(B, nv, nf, S, ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e =
+        cdk::launch_mesh_sample_backward(B, nv, nf, F, S, fidx, r1, r2, gP, gV, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_mesh_sample_backward launch");
+    return CD_OK;
+}
+
 }  // extern "C"

@@ -63,4 +63,18 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
                            const float *X, const float *Y, const int32_t *idx_xy,
                            const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream);
 
+// Mesh surface sampling (mesh_sample.hip).
+size_t mesh_workspace_bytes(int64_t B, int64_t nv, int64_t nf, int64_t S);
+hipError_t launch_mesh_choose_faces(int64_t B, int64_t nv, int64_t nf, const float *V,
+                                    const int32_t *F, int64_t S, const float *u, int32_t *fidx,
+                                    void *ws, hipStream_t stream);
+hipError_t launch_mesh_sample_points(int64_t B, int64_t nv, int64_t nf, const float *V,
+                                     const int32_t *F, int64_t S, const int32_t *fidx,
+                                     const float *r1, const float *r2, float *P,
+                                     hipStream_t stream);
+hipError_t launch_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const int32_t *F,
+                                       int64_t S, const int32_t *fidx, const float *r1,
+                                       const float *r2, const float *gP, float *gV, void *ws,
+                                       hipStream_t stream);
+
 }  // namespace cdk

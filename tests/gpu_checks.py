@@ -25,7 +25,7 @@ U32 = 2.0 ** -24
 
 
 def to_gpu(a: np.ndarray) -> torch.Tensor:
-    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+    return torch.from_numpy(np.array(a, copy=True, order="C")).to("cuda:0")
 
 
 def to_np(t: torch.Tensor) -> np.ndarray:

@@ -140,6 +140,43 @@ def test_metrics_rejects_bad_args(lib):
     assert lib.cd_metrics(0, 3, 3, None, None, 1.0, 1.0, tp, 3, None, None, None, None, None) == CD_OK
 
 
+def test_mesh_entry_points_reject_bad_args(lib):
+    assert lib.cd_mesh_workspace_bytes(2, 30, 10, 100) >= 2 * 10 * 8
+    assert lib.cd_mesh_workspace_bytes(2, 30, 0, 100) == 0
+    assert lib.cd_mesh_workspace_bytes(-1, 30, 10, 100) == 0
+    # Chunked backward: partial sums for every chunk, bounded whatever S is.
+    assert lib.cd_mesh_workspace_bytes(16, 600, 200, 16384) >= 16 * 2 * 600 * 24
+    for nv in (1, 600, 2048, 2049, 10 ** 6):
+        for B in (1, 3, 16):
+            w = lib.cd_mesh_workspace_bytes(B, nv, 10, (2 ** 31 - 1) // B)
+            assert 0 < w <= (48 << 20) + 256 and w % 256 == 0
+    assert lib.cd_mesh_workspace_bytes(2, 30, 10, 2 ** 30 + 1) == 0      # B * S > 2^31
+    ws = FAKE
+    assert lib.cd_mesh_sample_faces(1, 0, 4, FAKE, FAKE, 5, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_faces(1, 3, 0, FAKE, FAKE, 5, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_faces(1, 3, 4, FAKE, FAKE, -1, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_faces(4, 3, 4, FAKE, FAKE, 2 ** 29 + 1, FAKE, FAKE, ws, 1 << 40,
+                                    None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_faces(1, 3, 4, None, FAKE, 5, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_faces(1, 3, 4, FAKE, FAKE, 5, FAKE, FAKE, ws, 8, None) == CD_ERR_WORKSPACE
+    assert lib.cd_mesh_sample_faces(0, 3, 4, None, None, 5, None, None, None, 0, None) == CD_OK
+    for k in range(6):
+        a = [FAKE] * 6
+        a[k] = None
+        V, F, fi, r1, r2, P = a
+        assert lib.cd_mesh_sample_points(1, 3, 4, V, F, 5, fi, r1, r2, P, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_points(1, 3, 4, None, None, 0, None, None, None, None, None) == CD_OK
+    for k in range(6):
+        a = [FAKE] * 6
+        a[k] = None
+        F, fi, r1, r2, gP, gV = a
+        assert lib.cd_mesh_sample_backward(1, 3, 4, F, 5, fi, r1, r2, gP, gV, ws, 1 << 20,
+                                           None) == CD_ERR_INVALID_ARG
+    need = lib.cd_mesh_workspace_bytes(4, 600, 200, 16384)
+    assert lib.cd_mesh_sample_backward(4, 600, 200, FAKE, 16384, FAKE, FAKE, FAKE, FAKE, FAKE, ws,
+                                       need - 1, None) == CD_ERR_WORKSPACE
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     import paper_1911_05063_amd as cd
