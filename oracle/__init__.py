@@ -15,6 +15,9 @@ Two independent implementations live here:
 * ``mesh_oracle.c``: differentiable surface sampling of triangle meshes
   (Kaolin Sec. 2.1, reparameterization trick): area-weighted face choice,
   reparameterised points and their backward to the vertices, in double.
+* ``p2s_oracle.c``: the point-to-surface distance of Kaolin Sec. 2.5 (points
+  to the closest face of a triangle mesh), its face choice and its backward
+  to the points and vertices, in double.
 
 Every function follows Kaolin Sec. 2.5 (Chamfer distance for point clouds,
 defined through its citation of Fan et al.) under the readings listed in the
@@ -33,6 +36,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cd_oracle.c")
 _MESH_SRC = os.path.join(_HERE, "mesh_oracle.c")
+_P2S_SRC = os.path.join(_HERE, "p2s_oracle.c")
+# Every C source of the oracle library, in link order.
+SOURCES = (_SRC, _MESH_SRC, _P2S_SRC)
 LIB_PATH = os.path.join(_HERE, "libcd_oracle.so")
 
 _lib = None
@@ -41,7 +47,7 @@ _lib = None
 def build(verbose: bool = False) -> str:
     """Compile the C oracle (gcc, no FP contraction, OpenMP) into oracle/libcd_oracle.so."""
     cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
-           "-fPIC", "-shared", _SRC, _MESH_SRC, "-o", LIB_PATH + ".tmp", "-lm"]
+           "-fPIC", "-shared", *SOURCES, "-o", LIB_PATH + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
@@ -69,6 +75,9 @@ def _load():
     lib.oracle_sample_faces.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp]
     lib.oracle_sample_points.argtypes = [i64, i64, i64, vp, vp, i64, vp, vp, vp, vp]
     lib.oracle_sample_backward.argtypes = [i64, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp]
+    lib.oracle_point_triangle_batch.argtypes = [i64, vp, vp, vp, vp, vp, vp]
+    lib.oracle_p2s_forward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp]
+    lib.oracle_p2s_backward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -240,3 +249,57 @@ def sample_backward(V, F, fidx, r1, r2, gP):
     _load().oracle_sample_backward(B, V.shape[1], F.shape[1], _ptr(F), S, _ptr(fidx), _ptr(r1),
                                    _ptr(r2), _ptr(gP), _ptr(gV), _ptr(sV), _ptr(nV))
     return gV, sV, nV
+
+
+# ---------------------------------------------------------------- point to surface
+# Kaolin Sec. 2.5: point-to-surface loss for meshes (squared distance from each
+# point to the closest face, mean over the points).
+
+def point_triangle(p, a, b, c):
+    """(d2 [n], w [n, 3]): squared distance from p[k] to the closed triangle
+    (a[k], b[k], c[k]) and the barycentric coordinates of the closest point;
+    all inputs [n, 3], rounded to float32 first."""
+    p, a, b, c = (np.ascontiguousarray(np.reshape(x, (-1, 3)), np.float32) for x in (p, a, b, c))
+    n = p.shape[0]
+    if not (a.shape[0] == b.shape[0] == c.shape[0] == n):
+        raise ValueError("p, a, b, c must have the same number of rows")
+    d2 = np.empty(n, np.float64)
+    w = np.empty((n, 3), np.float64)
+    _load().oracle_point_triangle_batch(n, _ptr(p), _ptr(a), _ptr(b), _ptr(c), _ptr(d2), _ptr(w))
+    return d2, w
+
+
+def p2s_forward(P, V, F):
+    """(dist [B, S] float64, fidx [B, S] int32, w [B, S, 3] float64): squared
+    distance from every point to the closest face (lowest index on exact
+    ties) and the barycentric coordinates of the closest point."""
+    V, F = _mesh(V, F)
+    P = np.ascontiguousarray(P, np.float32)
+    if P.ndim != 3 or P.shape[2] != 3 or P.shape[0] != V.shape[0]:
+        raise ValueError("expected P [B, S, 3]")
+    B, S = P.shape[:2]
+    dist = np.empty((B, S), np.float64)
+    fidx = np.empty((B, S), np.int32)
+    w = np.empty((B, S, 3), np.float64)
+    _load().oracle_p2s_forward(B, S, V.shape[1], F.shape[1], _ptr(P), _ptr(V), _ptr(F),
+                               _ptr(dist), _ptr(fidx), _ptr(w))
+    return dist, fidx, w
+
+
+def p2s_backward(P, V, F, fidx, g):
+    """(gP [B, S, 3], gV [B, nv, 3], sV, nV) for the given face choices and
+    per-point weights g [B, S] = dL/d dist, in float64."""
+    V, F = _mesh(V, F)
+    P = np.ascontiguousarray(P, np.float32)
+    fidx = np.ascontiguousarray(fidx, np.int32)
+    g = np.ascontiguousarray(np.broadcast_to(g, fidx.shape), np.float64)
+    B, S = fidx.shape
+    if P.shape != (B, S, 3) or P.shape[0] != V.shape[0]:
+        raise ValueError("P and fidx shapes disagree")
+    gP = np.empty((B, S, 3), np.float64)
+    gV = np.empty(V.shape, np.float64)
+    sV = np.empty(V.shape, np.float64)
+    nV = np.empty(V.shape[:2], np.int32)
+    _load().oracle_p2s_backward(B, S, V.shape[1], F.shape[1], _ptr(P), _ptr(V), _ptr(F),
+                                _ptr(fidx), _ptr(g), _ptr(gP), _ptr(gV), _ptr(sV), _ptr(nV))
+    return gP, gV, sV, nV

@@ -33,7 +33,7 @@ from typing import Dict, Tuple
 import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "generate", "workload", "lattice_pair", "triangle_soup",
-           "grid_mesh", "uniforms"]
+           "grid_mesh", "uniforms", "icosphere", "p2s_workload", "P2S_WORKLOAD"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -247,3 +247,70 @@ def uniforms(B: int, S: int, seed: int, count: int = 3):
         u = rng.random((B, S)).astype(np.float32)
         out.append(np.minimum(u, np.float32(np.nextafter(np.float32(1), np.float32(0)))))
     return tuple(out)
+
+
+def icosphere(level: int):
+    """Unit icosphere: the icosahedron with each face split into 4 (edge
+    midpoints pushed to the sphere) `level` times.  Returns V [nv, 3] float64,
+    F [nf, 3] int32 with outward (counter-clockwise) faces; level 4 gives 2562
+    vertices and 5120 faces, the initial mesh of sphere-deforming
+    reconstruction networks."""
+    t = (1.0 + 5.0 ** 0.5) / 2.0
+    verts = [(-1, t, 0), (1, t, 0), (-1, -t, 0), (1, -t, 0), (0, -1, t), (0, 1, t),
+             (0, -1, -t), (0, 1, -t), (t, 0, -1), (t, 0, 1), (-t, 0, -1), (-t, 0, 1)]
+    verts = [np.array(v, dtype=np.float64) / np.linalg.norm(v) for v in verts]
+    faces = [(0, 11, 5), (0, 5, 1), (0, 1, 7), (0, 7, 10), (0, 10, 11), (1, 5, 9), (5, 11, 4),
+             (11, 10, 2), (10, 7, 6), (7, 1, 8), (3, 9, 4), (3, 4, 2), (3, 2, 6), (3, 6, 8),
+             (3, 8, 9), (4, 9, 5), (2, 4, 11), (6, 2, 10), (8, 6, 7), (9, 8, 1)]
+    for _ in range(level):
+        mid = {}
+
+        def midpoint(i, j):
+            key = (min(i, j), max(i, j))
+            if key not in mid:
+                m = verts[i] + verts[j]
+                verts.append(m / np.linalg.norm(m))
+                mid[key] = len(verts) - 1
+            return mid[key]
+
+        nxt = []
+        for a, b, c in faces:
+            ab, bc, ca = midpoint(a, b), midpoint(b, c), midpoint(c, a)
+            nxt += [(a, ab, ca), (b, bc, ab), (c, ca, bc), (ab, bc, ca)]
+        faces = nxt
+    return np.array(verts), np.array(faces, dtype=np.int32)
+
+
+@dataclasses.dataclass(frozen=True)
+class P2SWorkload:
+    """Point-to-surface workload: B deformed icospheres and B point clouds."""
+
+    name: str
+    B: int
+    S: int
+    level: int
+    seed: int
+
+
+P2S_WORKLOAD = P2SWorkload("p2s_b16_s16384_f5120", 16, 16384, 4, 6)
+
+
+def p2s_workload(B: int = 16, S: int = 16384, level: int = 4, seed: int = 6,
+                 noise: float = 0.05, jitter: float = 0.01):
+    """Point-to-surface inputs standing in for mesh reconstruction with a
+    point-to-surface loss: per item, an icosphere of radius U(0.8, 1.2) whose
+    vertices move radially by N(0, noise^2) (the predicted mesh), and S points
+    on an independently drawn radius-U(0.8, 1.2) sphere with N(0, jitter^2)
+    jitter (the target surface's samples).  Returns P [B, S, 3], V [B, nv, 3]
+    float32 and F [B, nf, 3] int32."""
+    V0, F0 = icosphere(level)
+    rng = np.random.default_rng(seed)
+    V = np.empty((B,) + V0.shape)
+    P = np.empty((B, S, 3))
+    for b in range(B):
+        r = rng.uniform(0.8, 1.2)
+        V[b] = V0 * (r + rng.normal(0.0, noise, (len(V0), 1)))
+        rp = rng.uniform(0.8, 1.2)
+        P[b] = rp * _unit_directions(rng, S) + rng.normal(0.0, jitter, (S, 3))
+    F = np.broadcast_to(F0, (B,) + F0.shape)
+    return _f32(P), _f32(V), np.ascontiguousarray(F)

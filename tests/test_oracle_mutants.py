@@ -43,9 +43,9 @@ def _mutant_module(tmp_path, name, src):
     c_path = tmp_path / f"{name}.c"
     so_path = tmp_path / f"{name}.so"
     c_path.write_text(src)
-    mesh_src = os.path.join(os.path.dirname(oracle.__file__), "mesh_oracle.c")
+    srcs = [str(c_path) if os.path.basename(x) == "cd_oracle.c" else x for x in oracle.SOURCES]
     subprocess.run(["gcc", "-O1", "-std=c11", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
-                    str(c_path), mesh_src, "-o", str(so_path), "-lm"], check=True)
+                    *srcs, "-o", str(so_path), "-lm"], check=True)
     spec = importlib.util.spec_from_file_location(f"oracle_{name}", oracle.__file__)
     mod = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(mod)
