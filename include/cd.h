@@ -213,6 +213,46 @@ cd_status cd_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const int32
                                   const float *r2, const float *gP, float *gV, void *ws,
                                   size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Point-to-surface distance (Kaolin Sec. 2.5: the point-to-surface loss for
+ * meshes, listed beside the Chamfer distance).  Per item b: points P [B, S, 3]
+ * float32, vertices V [B, nv, 3] float32, faces F [B, nf, 3] int32.  The
+ * distance of a point to a face is the squared Euclidean distance to the
+ * closed triangle; the loss of an item is the mean over its points of the
+ * distance to the nearest face (cd_reduce with w1 = 1, w2 = 0 computes it).
+ * Faces with a vertex index outside [0, nv) are ignored.  Checks (else
+ * CD_ERR_INVALID_ARG, nothing launched): B >= 0, S >= 0, nv >= 1, nf >= 1,
+ * nv, nf, S < 2^31, B * S <= 2^31, B * nf <= 2^31, B * ceil(nv / 2048) <= 2^23.
+ * B == 0 or S == 0 is a no-op (the backward still writes gV = 0 when S == 0).
+ */
+
+/* Device workspace bytes for cd_p2s_forward and cd_p2s_backward (one buffer
+ * serves both); 0 for sizes the checks reject. */
+size_t cd_p2s_workspace_bytes(int64_t B, int64_t S, int64_t nv, int64_t nf);
+
+/*
+ * dist [B, S] float32: squared distance from each point to the nearest face,
+ * evaluated in float32; fidx [B, S] int32: that face, the lowest index among
+ * exactly equal float32 distances; +inf and -1 when every face is ignored.
+ * ws: cd_p2s_workspace_bytes(B, S, nv, nf) bytes, 256-byte aligned.
+ */
+cd_status cd_p2s_forward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                         const float *V, const int32_t *F, float *dist, int32_t *fidx, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward for the faces fidx chosen by the forward and g [B, S] = dL/d dist:
+ * with q the closest point of face fidx to p (recomputed in double) and w its
+ * barycentric coordinates, gP = 2 g (p - q) [B, S, 3] and
+ * gV [B, nv, 3] = sum over points of -2 g w_i (p - q) on the face's vertex i
+ * (exact fixed-point sums as in cd_mesh_sample_backward: bitwise
+ * reproducible).  gP or gV may be NULL (not computed); both are fully
+ * overwritten.  Points whose face is out of range get gP = 0.
+ */
+cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                          const float *V, const int32_t *F, const int32_t *fidx, const float *g,
+                          float *gP, float *gV, void *ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

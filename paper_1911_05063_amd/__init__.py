@@ -15,6 +15,8 @@ Functions (names follow the C ABI):
   chamfer_distance(X, Y, w1, w2)    -> chamfer [B], differentiable (autograd)
   mesh_sample_faces / mesh_sample_points / mesh_sample_backward
                                     -> differentiable mesh surface sampling (Sec. 2.1)
+  p2s_forward / p2s_backward / point_to_surface
+                                    -> point-to-surface distance to triangle meshes (Sec. 2.5)
   sample_points(V, F, S)            -> P [B, S, 3], differentiable in V (autograd)
 """
 from __future__ import annotations
@@ -29,7 +31,8 @@ __all__ = [
     "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "chamfer_reduce",
     "f_score", "metrics", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
     "ChamferDistance", "forward_step", "mesh_sample_faces", "mesh_sample_points",
-    "mesh_sample_backward", "MeshSample", "sample_points",
+    "mesh_sample_backward", "MeshSample", "sample_points", "p2s_forward", "p2s_backward",
+    "PointToSurface", "point_to_surface",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcd_hip.so")
@@ -78,6 +81,13 @@ def library() -> ctypes.CDLL:
     lib.cd_mesh_sample_backward.restype = st
     lib.cd_mesh_sample_backward.argtypes = [i64, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp,
                                             ctypes.c_size_t, vp]
+    lib.cd_p2s_workspace_bytes.restype = ctypes.c_size_t
+    lib.cd_p2s_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.cd_p2s_forward.restype = st
+    lib.cd_p2s_forward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.cd_p2s_backward.restype = st
+    lib.cd_p2s_backward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp,
+                                    ctypes.c_size_t, vp]
     lib.cd_backward_pointwise.restype = st
     lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     _lib = lib
@@ -347,3 +357,77 @@ def sample_points(V: torch.Tensor, F: torch.Tensor, num_samples: int, generator=
                  for _ in range(3))
     fidx = mesh_sample_faces(V.detach(), F, u)
     return MeshSample.apply(V, F, fidx, r1, r2), fidx
+
+
+# ---------------------------------------------------------------- point to surface
+
+def _p2s_args(P, V, F):
+    V, F = _mesh(V, F)
+    P = _device_tensor(P, "P", torch.float32)
+    if P.dim() != 3 or P.shape[2] != 3 or P.shape[0] != V.shape[0] or P.device != V.device:
+        raise ValueError("expected P [B, S, 3] float32 on the mesh's device")
+    return P, V, F
+
+
+def _p2s_ws(B, S, nv, nf, device):
+    need = int(library().cd_p2s_workspace_bytes(B, S, nv, nf))
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+
+def p2s_forward(P, V, F):
+    """(dist [B, S], fidx [B, S]): squared distance from every point to the
+    nearest face of its item's mesh, and that face (Sec. 2.5)."""
+    P, V, F = _p2s_args(P, V, F)
+    B, S, nv, nf = P.shape[0], P.shape[1], V.shape[1], F.shape[1]
+    dist = torch.empty((B, S), dtype=torch.float32, device=P.device)
+    fidx = torch.empty((B, S), dtype=torch.int32, device=P.device)
+    ws = _p2s_ws(B, S, nv, nf, P.device)
+    with torch.cuda.device(P.device):
+        _check(library().cd_p2s_forward(B, S, nv, nf, _ptr(P), _ptr(V), _ptr(F), _ptr(dist),
+                                        _ptr(fidx), _ptr(ws), ws.numel(),
+                                        ctypes.c_void_p(_stream(P.device))), "cd_p2s_forward")
+    return dist, fidx
+
+
+def p2s_backward(P, V, F, fidx, g, want_points: bool = True, want_vertices: bool = True):
+    """(gP [B, S, 3] or None, gV [B, nv, 3] or None) for g [B, S] = dL/d dist."""
+    P, V, F = _p2s_args(P, V, F)
+    fidx = _device_tensor(fidx, "fidx", torch.int32)
+    g = _device_tensor(g, "g", torch.float32)
+    B, S, nv, nf = P.shape[0], P.shape[1], V.shape[1], F.shape[1]
+    gP = torch.empty((B, S, 3), dtype=torch.float32, device=P.device) if want_points else None
+    gV = torch.empty((B, nv, 3), dtype=torch.float32, device=P.device) if want_vertices else None
+    ws = _p2s_ws(B, S, nv, nf, P.device)
+    with torch.cuda.device(P.device):
+        _check(library().cd_p2s_backward(B, S, nv, nf, _ptr(P), _ptr(V), _ptr(F), _ptr(fidx),
+                                         _ptr(g), _ptr(gP) if gP is not None else None,
+                                         _ptr(gV) if gV is not None else None, _ptr(ws),
+                                         ws.numel(), ctypes.c_void_p(_stream(P.device))),
+               "cd_p2s_backward")
+    return gP, gV
+
+
+class PointToSurface(torch.autograd.Function):
+    """dist [B, S] = squared distance of each point to the nearest face,
+    differentiable in the points and the vertices (the face choice is not)."""
+
+    @staticmethod
+    def forward(ctx, P, V, F):
+        dist, fidx = p2s_forward(P, V, F)
+        ctx.save_for_backward(P, V, F, fidx)
+        ctx.mark_non_differentiable(fidx)
+        return dist, fidx
+
+    @staticmethod
+    def backward(ctx, g_dist, _g_fidx):
+        P, V, F, fidx = ctx.saved_tensors
+        gP, gV = p2s_backward(P, V, F, fidx, g_dist.contiguous().float(),
+                              want_points=ctx.needs_input_grad[0],
+                              want_vertices=ctx.needs_input_grad[1])
+        return gP, gV, None
+
+
+def point_to_surface(P, V, F):
+    """Per-point squared distances [B, S] (autograd); the point-to-surface loss
+    of Sec. 2.5 is their mean over the points."""
+    return PointToSurface.apply(P, V, F)[0]

@@ -264,4 +264,64 @@ cd_status cd_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const int32
     return CD_OK;
 }
 
+static cd_status check_p2s(int64_t B, int64_t S, int64_t nv, int64_t nf)
+{
+    if (B < 0) return invalid("B < 0");
+    if (S < 0) return invalid("S < 0");
+    if (nv < 1 || nf < 1) return invalid("a mesh needs nv >= 1 and nf >= 1");
+    if (nv > kMaxPoints || nf > kMaxPoints || S > kMaxPoints) return invalid("nv, nf or S >= 2^31");
+    if (B > 0 && (B * S > (int64_t(1) << 31) || B * nf > (int64_t(1) << 31) ||
+                  B * ((nv + 2047) / 2048) > (int64_t(1) << 23)))
+        return invalid("B * S > 2^31, B * nf > 2^31 or B * ceil(nv / 2048) > 2^23");
+    return CD_OK;
+}
+
+static cd_status check_ws(size_t need, const void *ws, size_t ws_bytes)
+{
+    if (!ws || ws_bytes < need) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
+        return CD_ERR_WORKSPACE;
+    }
+    if (!aligned256(ws)) return invalid("workspace not 256-byte aligned");
+    return CD_OK;
+}
+
+size_t cd_p2s_workspace_bytes(int64_t B, int64_t S, int64_t nv, int64_t nf)
+{
+    if (check_p2s(B, S, nv, nf) != CD_OK) return 0;
+    return (cdk::p2s_workspace_bytes(B, S, nv, nf) + 255) & ~static_cast<size_t>(255);
+}
+
+cd_status cd_p2s_forward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                         const float *V, const int32_t *F, float *dist, int32_t *fidx, void *ws,
+                         size_t ws_bytes, hipStream_t stream)
+{
+    cd_status s = check_p2s(B, S, nv, nf);
+    if (s != CD_OK) return s;
+    if (B == 0 || S == 0) return CD_OK;
+    if (!P || !V || !F || !dist || !fidx) return invalid("NULL array pointer");
+    s = check_ws(cd_p2s_workspace_bytes(B, S, nv, nf), ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e = cdk::launch_p2s_forward(B, S, nv, nf, P, V, F, dist, fidx, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_p2s_forward launch");
+    return CD_OK;
+}
+
+cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                          const float *V, const int32_t *F, const int32_t *fidx, const float *g,
+                          float *gP, float *gV, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    cd_status s = check_p2s(B, S, nv, nf);
+    if (s != CD_OK) return s;
+    if (B == 0 || (!gP && !gV)) return CD_OK;
+    if (!F || (S > 0 && (!P || !V || !fidx || !g))) return invalid("NULL array pointer");
+    s = check_ws(cd_p2s_workspace_bytes(B, S, nv, nf), ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e =
+        cdk::launch_p2s_backward(B, S, nv, nf, P, V, F, fidx, g, gP, gV, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_p2s_backward launch");
+    return CD_OK;
+}
+
 }  // extern "C"

@@ -63,6 +63,16 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
                            const float *X, const float *Y, const int32_t *idx_xy,
                            const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream);
 
+// Backward of barycentric interpolation onto mesh vertices (bary_scatter.hip):
+// gV[v] = sum of w_{s,v} gP[s] (negated if `negate`) over the samples whose
+// face holds v; weights from w [B, S, 3] if given, else from the sampling
+// uniforms (r1, r2).  ws: bary_scatter_workspace_bytes(B, nv, S) bytes.
+size_t bary_scatter_workspace_bytes(int64_t B, int64_t nv, int64_t S);
+hipError_t launch_bary_scatter(int64_t B, int64_t nv, int64_t nf, const int32_t *F, int64_t S,
+                               const int32_t *fidx, const float *r1, const float *r2,
+                               const float *w, const float *gP, bool negate, float *gV, void *ws,
+                               hipStream_t stream);
+
 // Mesh surface sampling (mesh_sample.hip).
 size_t mesh_workspace_bytes(int64_t B, int64_t nv, int64_t nf, int64_t S);
 hipError_t launch_mesh_choose_faces(int64_t B, int64_t nv, int64_t nf, const float *V,
@@ -76,5 +86,21 @@ hipError_t launch_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const 
                                        int64_t S, const int32_t *fidx, const float *r1,
                                        const float *r2, const float *gP, float *gV, void *ws,
                                        hipStream_t stream);
+
+// Point-to-surface distance (p2s.hip).  Points are cut into groups of 2048,
+// faces into blocks; one workgroup per (item, group, block).
+struct P2SPlan {
+    int nQG;   // point groups per item
+    int nFB;   // face blocks per item
+    int FB;    // faces per block
+};
+P2SPlan plan_p2s(int64_t B, int64_t S, int64_t nf);
+size_t p2s_workspace_bytes(int64_t B, int64_t S, int64_t nv, int64_t nf);
+hipError_t launch_p2s_forward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                              const float *V, const int32_t *F, float *dist, int32_t *fidx,
+                              void *ws, hipStream_t stream);
+hipError_t launch_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const float *P,
+                               const float *V, const int32_t *F, const int32_t *fidx,
+                               const float *g, float *gP, float *gV, void *ws, hipStream_t stream);
 
 }  // namespace cdk

@@ -196,3 +196,27 @@ def test_product_path_does_not_touch_the_oracle():
                 with open(os.path.join(dirpath, fn)) as f:
                     src = f.read()
                 assert "oracle" not in src.replace("oracle-free", ""), fn
+
+
+def test_p2s_entry_points_reject_bad_args(lib):
+    assert lib.cd_p2s_workspace_bytes(2, 100, 30, 10) > 0
+    assert lib.cd_p2s_workspace_bytes(2, 100, 30, 0) == 0
+    assert lib.cd_p2s_workspace_bytes(2, -1, 30, 10) == 0
+    assert lib.cd_p2s_workspace_bytes(2, 2 ** 30 + 1, 30, 10) == 0       # B * S > 2^31
+    assert lib.cd_p2s_workspace_bytes(16, 16384, 2562, 5120) % 256 == 0
+    ws = FAKE
+    for k in range(5):
+        a = [FAKE] * 5
+        a[k] = None
+        P, V, F, d, fi = a
+        assert lib.cd_p2s_forward(1, 5, 3, 1, P, V, F, d, fi, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_p2s_forward(1, 5, 0, 1, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_p2s_forward(1, 5, 3, 1, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 8, None) == CD_ERR_WORKSPACE
+    assert lib.cd_p2s_forward(0, 5, 3, 1, None, None, None, None, None, None, 0, None) == CD_OK
+    assert lib.cd_p2s_forward(2, 0, 3, 1, None, None, None, None, None, None, 0, None) == CD_OK
+    assert lib.cd_p2s_backward(1, 5, 3, 1, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ws, 1 << 30,
+                               None) == CD_OK                                  # nothing asked
+    assert lib.cd_p2s_backward(1, 5, 3, 1, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, ws, 1 << 30,
+                               None) == CD_ERR_INVALID_ARG
+    assert lib.cd_p2s_backward(1, 5, 3, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 8,
+                               None) == CD_ERR_WORKSPACE
