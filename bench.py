@@ -44,10 +44,12 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=100,
                     help="untimed steps; the GPU clock ramps up during the first ~50 ms")
     ap.add_argument("--workload", type=int, default=3, help="workload number 1..5 (default 3)")
-    ap.add_argument("--path", choices=("chamfer", "mesh"), default="chamfer",
+    ap.add_argument("--path", choices=("chamfer", "mesh", "p2s"), default="chamfer",
                     help="chamfer: the Chamfer step on the workload (default); mesh: the mesh "
                          "reconstruction loss step (surface sampling -> Chamfer -> vertex "
-                         "gradients) on 16 meshes of 200 triangles, 16384 samples each")
+                         "gradients) on 16 meshes of 200 triangles, 16384 samples each; "
+                         "p2s: the point-to-surface loss step on 16 deformed icospheres of "
+                         "5120 faces against 16384 points each")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
@@ -285,8 +287,119 @@ def mesh_step_bench(args):
     print(json.dumps(out), flush=True)
 
 
+# Point-to-surface pair function, counted on the straightforward evaluation
+# (an FMA counts 2): v = p - a (3); s, t and the normal offset h, three dot
+# products (15); u = 1 - s - t (2); inside test (3); three clamped segment
+# distances of 18 each (54); v - e0 for the third edge (3); minimum of the
+# edges (2); h^2 (1); selection (1); comparison with the best so far (1).
+P2S_FLOPS_PER_PAIR = 85
+
+
+def time_cpu_p2s(P, V, F, items, points):
+    """The oracle's point-to-surface forward + backward on a bounded sample:
+    the first `points` points of each of the first `items` items."""
+    import numpy as np
+    import oracle
+    Ps, Vs, Fs = P[:items, :points], V[:items], F[:items]
+    t0 = time.perf_counter()
+    dist, fidx, _ = oracle.p2s_forward(Ps, Vs, Fs)
+    oracle.p2s_backward(Ps, Vs, Fs, fidx, np.full(fidx.shape, 1.0 / points))
+    dt = time.perf_counter() - t0
+    pairs = float(items) * points * F.shape[1]
+    return {"value": pairs / dt, "unit": "point-triangle pair-evals/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"{items} items x {points} points x {F.shape[1]} faces, forward + backward, "
+                      f"OpenMP over points"}
+
+
+def p2s_step_bench(args):
+    """The point-to-surface loss step (Sec. 2.5): cd_p2s_forward, the per-item
+    mean (cd_reduce), cd_p2s_backward to the points and the vertices."""
+    import numpy as np
+    import torch
+    import paper_1911_05063_amd as cd
+    import synth
+
+    w = synth.P2S_WORKLOAD
+    P_np, V_np, F_np = synth.p2s_workload(w.B, w.S, w.level, w.seed)
+    B, S, nv, nf = w.B, w.S, V_np.shape[1], F_np.shape[1]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = lambda a: torch.from_numpy(np.array(a, copy=True)).to(dev)  # noqa: E731
+    P, V, F = g(P_np), g(V_np), g(F_np)
+    lib = cd.library()
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    ws = torch.empty(int(lib.cd_p2s_workspace_bytes(B, S, nv, nf)), dtype=torch.uint8, device=dev)
+    dist = torch.empty((B, S), dtype=torch.float32, device=dev)
+    fidx = torch.empty((B, S), dtype=torch.int32, device=dev)
+    loss = torch.empty(B, dtype=torch.float32, device=dev)
+    gdist = torch.full((B, S), 1.0 / S, dtype=torch.float32, device=dev)
+    gP = torch.empty_like(P)
+    gV = torch.empty_like(V)
+
+    def ok(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what}: {lib.cd_last_error().decode()}")
+
+    def one(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ok(lib.cd_p2s_forward(B, S, nv, nf, ptr(P), ptr(V), ptr(F), ptr(dist), ptr(fidx), ptr(ws),
+                              ws.numel(), st), "forward")
+        if ev is not None:
+            ev[1].record(stream)
+        ok(lib.cd_reduce(B, S, S, ptr(dist), ptr(dist), ctypes.c_float(1.0), ctypes.c_float(0.0),
+                         ptr(loss), st), "reduce")
+        ok(lib.cd_p2s_backward(B, S, nv, nf, ptr(P), ptr(V), ptr(F), ptr(fidx), ptr(gdist),
+                               ptr(gP), ptr(gV), ptr(ws), ws.numel(), st), "backward")
+        if ev is not None:
+            ev[2].record(stream)
+
+    print(f"[bench] {w.name}: B={B} S={S} nv={nv} nf={nf} steps={args.steps} "
+          f"warmup={args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(args.steps):
+        one(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
+    rest = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
+    pairs = float(B) * S * nf
+    achieved = P2S_FLOPS_PER_PAIR * pairs / (fwd * 1e-3) / 1e12
+    out = {"metric": "point-to-surface loss step point-triangle pair-evals/sec "
+                     "(forward + mean + backward to points and vertices)",
+           "value": pairs / (ms * 1e-3), "unit": "point-triangle pair-evals/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "S": S, "nv": nv, "nf": nf},
+           "ms_per_call": {"cd_p2s_forward": fwd, "reduce+backward": rest},
+           "roofline": {"bound": "alu", "kernel": "cd_p2s_forward (face records + search + merge)",
+                        "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                        "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+                        "work_per_launch": f"{P2S_FLOPS_PER_PAIR} flop x {pairs:.4g} "
+                                           f"point-triangle pairs"}}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = time_cpu_p2s(P_np, V_np, F_np, B, S // 2)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse_args()
+    if args.path == "p2s":
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        p2s_step_bench(args)
+        return
     if args.path == "mesh":
         if args.gpus != 1:
             print("bench.py measures one GPU only", file=sys.stderr)
