@@ -150,6 +150,8 @@ class Step:
         self.iyx = torch.empty((B, M), dtype=i32, device=dev)
         self.ws_bytes = int(self.lib.cd_workspace_bytes(B, N, M))
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+        self.bws_bytes = int(self.lib.cd_backward_workspace_bytes(B, N, M))
+        self.bws = torch.empty(self.bws_bytes, dtype=torch.uint8, device=dev)
         self.chamfer = torch.empty(B, dtype=f32, device=dev)
         self.taus = list(taus)
         self.fs = [torch.empty((len(self.taus), B), dtype=f32, device=dev) for _ in range(3)]
@@ -162,7 +164,8 @@ class Step:
         self.s = ctypes.c_void_p(self.stream.cuda_stream)
         P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
         self.p = {k: P(v) for k, v in dict(X=X, Y=Y, dxy=self.dxy, ixy=self.ixy, dyx=self.dyx,
-                                           iyx=self.iyx, ws=self.ws, ch=self.chamfer,
+                                           iyx=self.iyx, ws=self.ws, bws=self.bws,
+                                           ch=self.chamfer,
                                            go=self.grad_out, gX=self.gX, gY=self.gY,
                                            f=self.fs[0], pr=self.fs[1], rc=self.fs[2]).items()}
 
@@ -186,7 +189,8 @@ class Step:
     def backward(self):
         p = self.p
         self._ok(self.lib.cd_backward(self.B, self.N, self.M, p["go"], 1.0, 1.0, p["X"], p["Y"],
-                                      p["ixy"], p["iyx"], p["gX"], p["gY"], self.s), "cd_backward")
+                                      p["ixy"], p["iyx"], p["gX"], p["gY"], p["bws"],
+                                      self.bws_bytes, self.s), "cd_backward")
 
 
 def time_cpu_oracle(X, Y, taus, items):

@@ -126,6 +126,14 @@ cd_status cd_metrics(int64_t B, int64_t N, int64_t M,
                      float *f, float *precision, float *recall, hipStream_t stream);
 
 /*
+ * Device workspace bytes cd_backward and cd_backward_pointwise need for these
+ * sizes (per-block bounds, and per-chunk partial sums when a cloud's senders
+ * are split: at most a few hundred MB; 0 for B == 0 or sizes cd_forward
+ * rejects).
+ */
+size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
+
+/*
  * Backward of sum_b grad_out[b] * chamfer[b] (the Chamfer loss used to
  * supervise networks, Sec. 2.5), for the neighbours cd_forward chose:
  *   gX[b,i] = 2 g_xy (x_i - y_{idx_xy[i]}) - sum_{j: idx_yx[j]=i} 2 g_yx (y_j - x_i)
@@ -133,25 +141,32 @@ cd_status cd_metrics(int64_t B, int64_t N, int64_t M,
  * with g_xy = grad_out[b] * w1 / N and g_yx = grad_out[b] * w2 / M.
  *   grad_out [B]; X, Y, idx_xy, idx_yx as passed to / returned by cd_forward.
  *   gX [B,N,3], gY [B,M,3] are fully overwritten (not accumulated).
- * The scatter terms are added with float atomics, so the last bits may vary
- * from run to run.  A point whose index lies outside [0, M) / [0, N)
- * contributes nothing (its own and scatter terms are dropped).
+ *   ws: cd_backward_workspace_bytes(B, N, M) bytes, 256-byte aligned
+ *   (CD_ERR_WORKSPACE if smaller).
+ * Each term is evaluated in float32; the scatter sums are exact: every term is
+ * rounded to a 64-bit fixed-point integer (grid 2^-k, k per item and cloud
+ * from the largest term, about 2^-61 * (cloud size) times it) and the
+ * integers are added, so the result is bitwise reproducible run to run; own
+ * term + sum are added in double and rounded once.  A point whose index lies
+ * outside [0, M) / [0, N) contributes nothing (its own and scatter terms are
+ * dropped).
  */
 cd_status cd_backward(int64_t B, int64_t N, int64_t M, const float *grad_out,
                       float w1, float w2, const float *X, const float *Y,
                       const int32_t *idx_xy, const int32_t *idx_yx,
-                      float *gX, float *gY, hipStream_t stream);
+                      float *gX, float *gY, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Backward for an arbitrary loss of the nearest-neighbour distances:
  * g_xy [B,N] = dL/d dist_xy and g_yx [B,M] = dL/d dist_yx are given per point;
- * gX, gY are as in cd_backward with those per-point factors.
+ * gX, gY and ws are as in cd_backward with those per-point factors.
  */
 cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M,
                                 const float *g_xy, const float *g_yx,
                                 const float *X, const float *Y,
                                 const int32_t *idx_xy, const int32_t *idx_yx,
-                                float *gX, float *gY, hipStream_t stream);
+                                float *gX, float *gY, void *ws, size_t ws_bytes,
+                                hipStream_t stream);
 
 /*
  * Differentiable surface sampling of triangle meshes (Kaolin Sec. 2.1: mesh to

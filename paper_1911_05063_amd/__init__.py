@@ -71,7 +71,10 @@ def library() -> ctypes.CDLL:
     lib.cd_metrics.restype = st
     lib.cd_metrics.argtypes = [i64, i64, i64, vp, vp, f32, f32, vp, ctypes.c_int, vp, vp, vp, vp, vp]
     lib.cd_backward.restype = st
-    lib.cd_backward.argtypes = [i64, i64, i64, vp, f32, f32, vp, vp, vp, vp, vp, vp, vp]
+    lib.cd_backward_workspace_bytes.restype = ctypes.c_size_t
+    lib.cd_backward_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.cd_backward.argtypes = [i64, i64, i64, vp, f32, f32, vp, vp, vp, vp, vp, vp, vp,
+                                ctypes.c_size_t, vp]
     lib.cd_mesh_workspace_bytes.restype = ctypes.c_size_t
     lib.cd_mesh_workspace_bytes.argtypes = [i64, i64, i64, i64]
     lib.cd_mesh_sample_faces.restype = st
@@ -89,7 +92,8 @@ def library() -> ctypes.CDLL:
     lib.cd_p2s_backward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.cd_backward_pointwise.restype = st
-    lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                          ctypes.c_size_t, vp]
     _lib = lib
     return lib
 
@@ -198,6 +202,11 @@ def metrics(dist_xy: torch.Tensor, dist_yx: torch.Tensor, taus, w1: float = 1.0,
     return ch, f, p, r
 
 
+def _backward_ws(B, N, M, device):
+    need = int(library().cd_backward_workspace_bytes(B, N, M))
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+
 def chamfer_backward(grad_out: torch.Tensor, X: torch.Tensor, Y: torch.Tensor,
                      idx_xy: torch.Tensor, idx_yx: torch.Tensor, w1: float = 1.0,
                      w2: float = 1.0) -> Tuple[torch.Tensor, torch.Tensor]:
@@ -209,10 +218,12 @@ def chamfer_backward(grad_out: torch.Tensor, X: torch.Tensor, Y: torch.Tensor,
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
     gX = torch.empty_like(X)
     gY = torch.empty_like(Y)
+    ws = _backward_ws(B, N, M, X.device)
     with torch.cuda.device(X.device):
         _check(library().cd_backward(B, N, M, _ptr(go), float(w1), float(w2), _ptr(X), _ptr(Y),
-                                     _ptr(ixy), _ptr(iyx), _ptr(gX), _ptr(gY),
-                                     ctypes.c_void_p(_stream(X.device))), "cd_backward")
+                                     _ptr(ixy), _ptr(iyx), _ptr(gX), _ptr(gY), _ptr(ws),
+                                     ws.numel(), ctypes.c_void_p(_stream(X.device))),
+               "cd_backward")
     return gX, gY
 
 
@@ -228,9 +239,11 @@ def chamfer_backward_pointwise(g_xy: torch.Tensor, g_yx: torch.Tensor, X: torch.
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
     gX = torch.empty_like(X)
     gY = torch.empty_like(Y)
+    ws = _backward_ws(B, N, M, X.device)
     with torch.cuda.device(X.device):
         _check(library().cd_backward_pointwise(B, N, M, _ptr(gxy), _ptr(gyx), _ptr(X), _ptr(Y),
                                                _ptr(ixy), _ptr(iyx), _ptr(gX), _ptr(gY),
+                                               _ptr(ws), ws.numel(),
                                                ctypes.c_void_p(_stream(X.device))),
                "cd_backward_pointwise")
     return gX, gY

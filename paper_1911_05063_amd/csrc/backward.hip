@@ -5,22 +5,45 @@
 // for j = idx_xy[i]; symmetrically for dist_yx.  So
 //   gX[i] = 2 g_xy(i) (x_i - y_{idx_xy[i]}) - sum_{j: idx_yx[j] = i} 2 g_yx(j) (y_j - x_i)
 //   gY[j] = 2 g_yx(j) (y_j - x_{idx_yx[j]}) - sum_{i: idx_xy[i] = j} 2 g_xy(i) (x_i - y_j)
+// The first term is the point's own; the sum scatters the other cloud's
+// ("senders'") terms onto their neighbours ("receivers").
 //
-// One launch, no global atomics.  A workgroup owns a slice of kSlice points of
-// one cloud (the receiving side) of one item: it scans the other cloud's
-// neighbour indices, adds the scatter terms that land in its slice to LDS
-// accumulators (ds_add_f32), then writes own term + accumulated scatter once
-// per point.  Global float atomics on this chip are executed far from the CU
-// (about 20 G/s measured), LDS atomics next to it.  The order of the LDS
-// additions varies from run to run, so the last bits may too.
+// The scatter sums are exact and therefore bitwise reproducible: every
+// contribution (a float32 product) is rounded to a 64-bit fixed-point integer
+// and the integers are added, so their order does not matter.
+//  * bound_kernel: per block of 1024 points of an item, the bounding box of
+//    both clouds and the largest |dL/d dist|.  Every contribution component
+//    is at most 2 |g| times the box's largest extent, which gives the
+//    fixed-point shift (fixed_point.h) keeping every receiver's sum below
+//    2^62; the grid is then about 2^-61 * (cloud size) * 2 |g| * extent,
+//    far below float32 rounding of the terms.  Coalesced reads, no gathers.
+//  * scatter_kernel: a workgroup owns a slice of 2048 receivers of one cloud
+//    and item and a chunk of the other cloud's senders; it scans the chunk's
+//    neighbour indices (8 per thread per round, every load issued before the
+//    first wait) and adds the terms that land in its slice to LDS int64
+//    accumulators (ds_add_u64).  With one chunk per item it then writes
+//    own + scatter directly; otherwise the slice goes to the workspace.
+//  * finalize_kernel: per receiver, the chunks' integer partials summed
+//    exactly, scaled back, plus the own term (in double), rounded once.
+// Senders are split into chunks only on a side whose scan is much longer than
+// the other's (a few receivers, many senders: one cloud much larger).
+// A point whose neighbour index lies outside the other cloud contributes
+// nothing (its own term is 0 and it scatters nothing).
+#include <algorithm>
+
 #include "cd_internal.h"
+#include "fixed_point.h"
 
 namespace cdk {
 namespace {
 
-constexpr int kBlock = 512;
-constexpr int kSlice = 2048;
-constexpr int kUnroll = 8;
+constexpr int kBlock = 512;                 // threads of a scatter workgroup
+constexpr int kSlice = 2048;                // receivers per workgroup
+constexpr int kUnroll = 8;                  // senders per thread per round
+constexpr int64_t kRound = static_cast<int64_t>(kBlock) * kUnroll;
+constexpr int kBoundBlock = 1024;           // points per bound block
+constexpr int kBound = 8;                   // per block: -min xyz, max xyz, max|g_xy|, max|g_yx|
+constexpr int kThreads = 256;
 
 struct BwdArgs {
     const float *gxy;   // [B] (per item) or [B, N] (pointwise)
@@ -31,114 +54,334 @@ struct BwdArgs {
     const int32_t *idx_yx;
     float *gX;
     float *gY;
+    float *bpart;       // [B][nblk][kBound] per-block box and |g| maxima
+    int *shift;         // [B][2] fixed-point shift per item and receiving side
+    long long *part;    // per-chunk partial sums (sides with more than one chunk)
     int64_t B, N, M;
     float sxy, syx;     // per-item scale (w1/N, w2/M) when not pointwise
-    int pointwise;
-    int nsx, nsy;       // slices of X and of Y per item
+    int nblk;           // bound blocks per item (of the larger cloud)
+    int ns[2];          // receiving slices per item (side 0: X receives, 1: Y)
+    int nc[2];          // sender chunks per item
+    int64_t chunk[2];   // senders per chunk (a multiple of kRound)
+    int64_t poff[2];    // first partial of each side in part
 };
 
-// dL/d dist of point p (flat index) of cloud X (xdir) or Y, item b.
-__device__ __forceinline__ float weight(const BwdArgs &a, bool xdir, int64_t b, int64_t p)
+// The clouds as seen from receiving side `side` of item b, with the factors
+// 2 dL/d dist of senders and receivers: per point (gs, gr) if pointwise, else
+// one per item (g2s, g2r).
+struct Side {
+    const float *R;          // receivers [n_recv, 3]
+    const float *S;          // senders [n_send, 3]
+    const int32_t *sidx;     // sender -> receiver
+    const int32_t *ridx;     // receiver -> sender (its own neighbour)
+    float *out;              // [n_recv, 3]
+    const float *gs, *gr;    // [n_send], [n_recv] (pointwise)
+    float g2s, g2r;          // per item (not pointwise)
+    int64_t n_recv, n_send;
+};
+
+template <bool kPointwise>
+__device__ __forceinline__ Side side_of(const BwdArgs &a, int side, int64_t b)
 {
-    if (a.pointwise) return xdir ? a.gxy[p] : a.gyx[p];
-    return (xdir ? a.gxy[b] : a.gyx[b]) * (xdir ? a.sxy : a.syx);
+    Side s;
+    const bool xs = side == 0;
+    s.n_recv = xs ? a.N : a.M;
+    s.n_send = xs ? a.M : a.N;
+    s.R = (xs ? a.X : a.Y) + b * s.n_recv * 3;
+    s.S = (xs ? a.Y : a.X) + b * s.n_send * 3;
+    s.sidx = (xs ? a.idx_yx : a.idx_xy) + b * s.n_send;
+    s.ridx = (xs ? a.idx_xy : a.idx_yx) + b * s.n_recv;
+    s.out = (xs ? a.gX : a.gY) + b * s.n_recv * 3;
+    if (kPointwise) {
+        s.gs = (xs ? a.gyx : a.gxy) + b * s.n_send;
+        s.gr = (xs ? a.gxy : a.gyx) + b * s.n_recv;
+        s.g2s = s.g2r = 0.0f;
+    } else {
+        s.gs = s.gr = nullptr;
+        const float gx = 2.0f * (a.gxy[b] * a.sxy), gy = 2.0f * (a.gyx[b] * a.syx);
+        s.g2s = xs ? gy : gx;
+        s.g2r = xs ? gx : gy;
+    }
+    return s;
 }
 
-// Workgroup (b, side, slice).  side 0 writes gX[b, slice], side 1 gY[b, slice].
-__global__ __launch_bounds__(kBlock) void backward_kernel(BwdArgs a)
+template <bool kPointwise>
+__device__ __forceinline__ float g2_send(const Side &s, int64_t j)
 {
-    __shared__ float acc[3][kSlice];
-    const int per_item = a.nsx + a.nsy;
-    const int64_t b = blockIdx.x / per_item;
-    const int r = blockIdx.x % per_item;
-    const bool xside = r < a.nsx;                 // receiving cloud is X
-    const int64_t s0 = static_cast<int64_t>(xside ? r : r - a.nsx) * kSlice;
-    const int64_t nrecv = xside ? a.N : a.M;      // points of the receiving cloud
-    const int64_t nsend = xside ? a.M : a.N;      // points of the other cloud
-    const int64_t s1 = min(s0 + kSlice, nrecv);
-    const float *R = (xside ? a.X : a.Y) + b * nrecv * 3;              // receiving, item b
-    const float *S = (xside ? a.Y : a.X) + b * nsend * 3;              // sending, item b
-    const int32_t *sidx = (xside ? a.idx_yx : a.idx_xy) + b * nsend;   // sender -> receiver
-    const int32_t *ridx = (xside ? a.idx_xy : a.idx_yx) + b * nrecv;   // receiver -> sender
-    float *out = (xside ? a.gX : a.gY) + b * nrecv * 3;
+    return kPointwise ? 2.0f * s.gs[j] : s.g2s;
+}
 
-    for (int t = threadIdx.x; t < kSlice; t += kBlock) {
-        acc[0][t] = 0.0f;
-        acc[1][t] = 0.0f;
-        acc[2][t] = 0.0f;
+template <bool kPointwise>
+__device__ __forceinline__ float g2_recv(const Side &s, int64_t i)
+{
+    return kPointwise ? 2.0f * s.gr[i] : s.g2r;
+}
+
+template <bool kPointwise>
+__global__ __launch_bounds__(kBoundBlock) void bound_kernel(BwdArgs a)
+{
+    __shared__ float red[kBoundBlock / kWave];
+    const int64_t b = blockIdx.x / a.nblk;
+    const int64_t blk = blockIdx.x % a.nblk;
+    const int64_t j = blk * kBoundBlock + threadIdx.x;
+    // v[0..2] = -min, v[3..5] = max of the coordinates (so all are maxima).
+    float v[kBound];
+#pragma unroll
+    for (int c = 0; c < kBound; ++c) v[c] = -__builtin_inff();
+    v[6] = v[7] = 0.0f;
+    if (j < a.N) {
+        const float *x = a.X + (b * a.N + j) * 3;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            v[c] = fmaxf(v[c], -x[c]);
+            v[3 + c] = fmaxf(v[3 + c], x[c]);
+        }
+        v[6] = fabsf(kPointwise ? a.gxy[b * a.N + j] : a.gxy[b] * a.sxy);
     }
+    if (j < a.M) {
+        const float *y = a.Y + (b * a.M + j) * 3;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            v[c] = fmaxf(v[c], -y[c]);
+            v[3 + c] = fmaxf(v[3 + c], y[c]);
+        }
+        v[7] = fabsf(kPointwise ? a.gyx[b * a.M + j] : a.gyx[b] * a.syx);
+    }
+    float *out = a.bpart + (b * a.nblk + blk) * kBound;
+#pragma unroll
+    for (int c = 0; c < kBound; ++c) {
+        const float m = group_max<kBoundBlock>(v[c], red);
+        if (threadIdx.x == 0) out[c] = m;
+    }
+}
+
+// Own term of receiver p plus the scatter sum (double), rounded once.
+template <bool kPointwise>
+__device__ __forceinline__ void write_point(const BwdArgs &a, const Side &s, int side, int64_t b,
+                                            int64_t p, const double scat[3])
+{
+    const int32_t nb = s.ridx[p];
+    const bool ok = nb >= 0 && nb < s.n_send;
+    const int64_t qn = ok ? nb : 0;
+    const float g2 = ok ? g2_recv<kPointwise>(s, p) : 0.0f;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+        const float own = g2 * (s.R[3 * p + c] - s.S[3 * qn + c]);
+        s.out[3 * p + c] = static_cast<float>(static_cast<double>(own) + scat[c]);
+    }
+}
+
+template <bool kPointwise>
+__global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
+{
+    __shared__ unsigned long long acc[3 * kSlice];
+    __shared__ float red[kBlock / kWave];
+    const int64_t g0 = a.B * a.ns[0] * a.nc[0];
+    const int side = blockIdx.x < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int ns = a.ns[side], nc = a.nc[side];
+    const int64_t b = g / (static_cast<int64_t>(ns) * nc);
+    const int rest = static_cast<int>(g % (static_cast<int64_t>(ns) * nc));
+    const int slice = rest / nc, c = rest % nc;
+    const Side s = side_of<kPointwise>(a, side, b);
+    const int64_t r0 = static_cast<int64_t>(slice) * kSlice;
+    const int64_t r1 = std::min<int64_t>(r0 + kSlice, s.n_recv);
+
+    // The shift: every contribution component is at most 2 max|g_send| times
+    // the largest extent of the item's bounding box.
+    const float *bp = a.bpart + b * a.nblk * kBound;
+    float v[kBound];
+#pragma unroll
+    for (int c = 0; c < kBound; ++c) v[c] = -__builtin_inff();
+    for (int64_t k = threadIdx.x; k < a.nblk; k += kBlock) {
+#pragma unroll
+        for (int c = 0; c < kBound; ++c) v[c] = fmaxf(v[c], bp[k * kBound + c]);
+    }
+    float ext = 0.0f;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) ext = fmaxf(ext, v[3 + c] + v[c]);      // max - min
+    const float gs = side == 0 ? v[7] : v[6];                            // senders' |g|
+    const float m = 2.0f * gs * ext;
+    const int ks = fixed_shift(group_max<kBlock>(m, red), s.n_send);
+    if (slice == 0 && c == 0 && threadIdx.x == 0) a.shift[b * 2 + side] = ks;
+
+    for (int t = threadIdx.x; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
     __syncthreads();
 
-    // Scatter terms of senders whose neighbour lies in this slice:
-    // -2 g(s) (s - r) added to r.  kUnroll senders per thread per round, with
-    // every load issued before the first wait (out-of-slice lanes read a
-    // clamped, valid address and add nothing).
-    const bool spw = a.pointwise != 0;
-    const float g2s_item = spw ? 0.0f : 2.0f * weight(a, !xside, b, 0);
-    const float *gsend = (xside ? a.gyx : a.gxy) + (spw ? b * nsend : 0);  // [B, n] only if pointwise
-    for (int64_t base = 0; base < nsend; base += static_cast<int64_t>(kBlock) * kUnroll) {
+    // Scatter terms of this chunk's senders whose neighbour lies in the slice:
+    // -2 g(s) (s - r) added to r.  Out-of-slice lanes read a clamped, valid
+    // address and add nothing.
+    const int64_t q0 = c * a.chunk[side];
+    const int64_t q1 = std::min<int64_t>(q0 + a.chunk[side], s.n_send);
+    for (int64_t base = q0; base < q1; base += kRound) {
         int64_t qs[kUnroll], is[kUnroll];
         bool in[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int64_t q = base + static_cast<int64_t>(u) * kBlock + threadIdx.x;
-            qs[u] = min(q, nsend - 1);
-            const int64_t i = sidx[qs[u]];
-            in[u] = q < nsend && i >= s0 && i < s1;
-            is[u] = in[u] ? i : s0;
+            qs[u] = std::min<int64_t>(q, q1 - 1);
+            const int64_t i = s.sidx[qs[u]];
+            in[u] = q < q1 && i >= r0 && i < r1;
+            is[u] = in[u] ? i : r0;
         }
         float sv[kUnroll][3], rv[kUnroll][3], g2[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                sv[u][c] = S[3 * qs[u] + c];
-                rv[u][c] = R[3 * is[u] + c];
+            for (int d = 0; d < 3; ++d) {
+                sv[u][d] = s.S[3 * qs[u] + d];
+                rv[u][d] = s.R[3 * is[u] + d];
             }
-            g2[u] = spw ? 2.0f * gsend[qs[u]] : g2s_item;
+            g2[u] = g2_send<kPointwise>(s, qs[u]);
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (in[u]) {
-                const int64_t l = is[u] - s0;
+                unsigned long long *t = acc + 3 * (is[u] - r0);
 #pragma unroll
-                for (int c = 0; c < 3; ++c) atomicAdd(&acc[c][l], -(g2[u] * (sv[u][c] - rv[u][c])));
+                for (int d = 0; d < 3; ++d)
+                    atomicAdd(t + d, static_cast<unsigned long long>(
+                                         to_fixed(-(g2[u] * (sv[u][d] - rv[u][d])), ks)));
             }
         }
     }
     __syncthreads();
 
-    // Own term plus the accumulated scatter, written once per point.  A point
-    // whose neighbour index is out of range contributes nothing.
-    const float g2r_item = spw ? 0.0f : 2.0f * weight(a, xside, b, 0);
-    const float *grecv = (xside ? a.gxy : a.gyx) + (spw ? b * nrecv : 0);
-#pragma unroll 4
-    for (int64_t p = s0 + threadIdx.x; p < s1; p += kBlock) {
-        const int64_t l = p - s0;
-        const int32_t nb = ridx[p];
-        const bool ok = nb >= 0 && nb < nsend;
-        const int64_t qn = ok ? nb : 0;
-        const float g2 = ok ? (spw ? 2.0f * grecv[p] : g2r_item) : 0.0f;
-#pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            const float own = g2 * (R[3 * p + c] - S[3 * qn + c]);
-            out[3 * p + c] = own + acc[c][l];
+    if (nc == 1) {
+        for (int64_t p = r0 + threadIdx.x; p < r1; p += kBlock) {
+            const unsigned long long *t = acc + 3 * (p - r0);
+            const double scat[3] = {ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
+                                    ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
+                                    ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
+            write_point<kPointwise>(a, s, side, b, p, scat);
         }
+    } else {
+        long long *dst = a.part + a.poff[side] + ((b * nc + c) * s.n_recv + r0) * 3;
+        for (int t = threadIdx.x; t < 3 * (r1 - r0); t += kBlock)
+            dst[t] = static_cast<long long>(acc[t]);
     }
+}
+
+// Receivers of `side` (which has more than one chunk): exact sum of the
+// chunks' partials, own term added, rounded once.
+template <bool kPointwise>
+__global__ __launch_bounds__(kThreads) void finalize_kernel(BwdArgs a, int side)
+{
+    const int64_t n_recv = side == 0 ? a.N : a.M;
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    if (k >= a.B * n_recv) return;
+    const int64_t b = k / n_recv, p = k - b * n_recv;
+    const Side s = side_of<kPointwise>(a, side, b);
+    const int nc = a.nc[side];
+    const long long *src = a.part + a.poff[side] + (b * nc * n_recv + p) * 3;
+    unsigned long long sum[3] = {0ull, 0ull, 0ull};
+    for (int c = 0; c < nc; ++c) {
+#pragma unroll
+        for (int d = 0; d < 3; ++d)
+            sum[d] += static_cast<unsigned long long>(src[static_cast<int64_t>(c) * n_recv * 3 + d]);
+    }
+    const int ks = a.shift[b * 2 + side];
+    const double scat[3] = {ldexp(static_cast<double>(static_cast<long long>(sum[0])), -ks),
+                            ldexp(static_cast<double>(static_cast<long long>(sum[1])), -ks),
+                            ldexp(static_cast<double>(static_cast<long long>(sum[2])), -ks)};
+    write_point<kPointwise>(a, s, side, b, p, scat);
+}
+
+int64_t ceil_div(int64_t x, int64_t y) { return (x + y - 1) / y; }
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+struct BwdPlan {
+    int nblk;
+    int ns[2], nc[2];
+    int64_t chunk[2];
+    size_t bpart_bytes, shift_bytes, part_elems[2];
+};
+
+BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
+{
+    BwdPlan p;
+    p.nblk = static_cast<int>(ceil_div(std::max(N, M), kBoundBlock));
+    const int64_t n_recv[2] = {N, M}, n_send[2] = {M, N};
+    int64_t rounds[2];
+    for (int s = 0; s < 2; ++s) {
+        p.ns[s] = static_cast<int>(ceil_div(n_recv[s], kSlice));
+        rounds[s] = ceil_div(n_send[s], kRound);
+    }
+    // A side whose workgroups would scan many more rounds than the other's
+    // splits its senders into chunks of about the other's length (at least 2
+    // rounds): the long scan is what bounds the kernel's time otherwise.
+    const int64_t target = std::max<int64_t>(2, std::min(rounds[0], rounds[1]));
+    for (int s = 0; s < 2; ++s) {
+        const int64_t want = ceil_div(rounds[s], target);
+        p.chunk[s] = ceil_div(rounds[s], want) * kRound;
+        p.nc[s] = static_cast<int>(ceil_div(n_send[s], p.chunk[s]));
+        p.part_elems[s] = p.nc[s] > 1 ? static_cast<size_t>(B * p.nc[s] * n_recv[s] * 3) : 0;
+    }
+    p.bpart_bytes = align256(static_cast<size_t>(B * p.nblk) * kBound * 4);
+    p.shift_bytes = align256(static_cast<size_t>(B * 2) * 4);
+    return p;
 }
 
 }  // namespace
 
+size_t backward_workspace_bytes(int64_t B, int64_t N, int64_t M)
+{
+    const BwdPlan p = plan_backward(B, N, M);
+    return p.bpart_bytes + p.shift_bytes + align256((p.part_elems[0] + p.part_elems[1]) * 8);
+}
+
 hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
                            const float *g_yx, bool pointwise, float sxy, float syx,
                            const float *X, const float *Y, const int32_t *idx_xy,
-                           const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream)
+                           const int32_t *idx_yx, float *gX, float *gY, void *ws,
+                           hipStream_t stream)
 {
-    BwdArgs a{g_xy, g_yx, X, Y, idx_xy, idx_yx, gX, gY, B, N, M, sxy, syx, pointwise ? 1 : 0,
-              static_cast<int>((N + kSlice - 1) / kSlice),
-              static_cast<int>((M + kSlice - 1) / kSlice)};
-    const int64_t grid = B * (a.nsx + a.nsy);
-    backward_kernel<<<static_cast<uint32_t>(grid), kBlock, 0, stream>>>(a);
+    const BwdPlan p = plan_backward(B, N, M);
+    char *base = static_cast<char *>(ws);
+    BwdArgs a{};
+    a.gxy = g_xy;
+    a.gyx = g_yx;
+    a.X = X;
+    a.Y = Y;
+    a.idx_xy = idx_xy;
+    a.idx_yx = idx_yx;
+    a.gX = gX;
+    a.gY = gY;
+    a.bpart = reinterpret_cast<float *>(base);
+    a.shift = reinterpret_cast<int *>(base + p.bpart_bytes);
+    a.part = reinterpret_cast<long long *>(base + p.bpart_bytes + p.shift_bytes);
+    a.B = B;
+    a.N = N;
+    a.M = M;
+    a.sxy = sxy;
+    a.syx = syx;
+    a.nblk = p.nblk;
+    for (int s = 0; s < 2; ++s) {
+        a.ns[s] = p.ns[s];
+        a.nc[s] = p.nc[s];
+        a.chunk[s] = p.chunk[s];
+    }
+    a.poff[0] = 0;
+    a.poff[1] = static_cast<int64_t>(p.part_elems[0]);
+    const uint32_t nbound = static_cast<uint32_t>(B * p.nblk);
+    const int64_t groups = B * (static_cast<int64_t>(p.ns[0]) * p.nc[0] +
+                                static_cast<int64_t>(p.ns[1]) * p.nc[1]);
+    if (pointwise) {
+        bound_kernel<true><<<nbound, kBoundBlock, 0, stream>>>(a);
+        scatter_kernel<true><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
+    } else {
+        bound_kernel<false><<<nbound, kBoundBlock, 0, stream>>>(a);
+        scatter_kernel<false><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
+    }
+    for (int s = 0; s < 2; ++s) {
+        if (p.nc[s] <= 1) continue;
+        const uint32_t grid = static_cast<uint32_t>(ceil_div(B * (s == 0 ? N : M), kThreads));
+        if (pointwise)
+            finalize_kernel<true><<<grid, kThreads, 0, stream>>>(a, s);
+        else
+            finalize_kernel<false><<<grid, kThreads, 0, stream>>>(a, s);
+    }
     return hipGetLastError();
 }
 

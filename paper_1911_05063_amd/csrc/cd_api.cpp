@@ -153,19 +153,41 @@ cd_status cd_metrics(int64_t B, int64_t N, int64_t M, const float *dist_xy, cons
     return CD_OK;
 }
 
+size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M)
+{
+    if (check_shape(B, N, M) != CD_OK || B == 0) return 0;
+    return (cdk::backward_workspace_bytes(B, N, M) + 255) & ~static_cast<size_t>(255);
+}
+
+static cd_status check_backward_ws(int64_t B, int64_t N, int64_t M, const void *ws,
+                                   size_t ws_bytes)
+{
+    const size_t need = cd_backward_workspace_bytes(B, N, M);
+    if (!ws || ws_bytes < need) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
+        return CD_ERR_WORKSPACE;
+    }
+    if (!aligned256(ws)) return invalid("workspace not 256-byte aligned");
+    return CD_OK;
+}
+
 cd_status cd_backward(int64_t B, int64_t N, int64_t M, const float *grad_out, float w1, float w2,
                       const float *X, const float *Y, const int32_t *idx_xy,
-                      const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream)
+                      const int32_t *idx_yx, float *gX, float *gY, void *ws, size_t ws_bytes,
+                      hipStream_t stream)
 {
     cd_status s = check_shape(B, N, M);
     if (s != CD_OK) return s;
     if (B == 0) return CD_OK;
     if (!grad_out || !X || !Y || !idx_xy || !idx_yx || !gX || !gY)
         return invalid("NULL array pointer");
+    s = check_backward_ws(B, N, M, ws, ws_bytes);
+    if (s != CD_OK) return s;
     const float sxy = static_cast<float>(static_cast<double>(w1) / static_cast<double>(N));
     const float syx = static_cast<float>(static_cast<double>(w2) / static_cast<double>(M));
     const hipError_t e = cdk::launch_backward(B, N, M, grad_out, grad_out, false, sxy, syx, X, Y,
-                                              idx_xy, idx_yx, gX, gY, stream);
+                                              idx_xy, idx_yx, gX, gY, ws, stream);
     if (e != hipSuccess) return hip_failed(e, "cd_backward launch");
     return CD_OK;
 }
@@ -173,15 +195,17 @@ cd_status cd_backward(int64_t B, int64_t N, int64_t M, const float *grad_out, fl
 cd_status cd_backward_pointwise(int64_t B, int64_t N, int64_t M, const float *g_xy,
                                 const float *g_yx, const float *X, const float *Y,
                                 const int32_t *idx_xy, const int32_t *idx_yx, float *gX,
-                                float *gY, hipStream_t stream)
+                                float *gY, void *ws, size_t ws_bytes, hipStream_t stream)
 {
     cd_status s = check_shape(B, N, M);
     if (s != CD_OK) return s;
     if (B == 0) return CD_OK;
     if (!g_xy || !g_yx || !X || !Y || !idx_xy || !idx_yx || !gX || !gY)
         return invalid("NULL array pointer");
+    s = check_backward_ws(B, N, M, ws, ws_bytes);
+    if (s != CD_OK) return s;
     const hipError_t e = cdk::launch_backward(B, N, M, g_xy, g_yx, true, 1.0f, 1.0f, X, Y, idx_xy,
-                                              idx_yx, gX, gY, stream);
+                                              idx_yx, gX, gY, ws, stream);
     if (e != hipSuccess) return hip_failed(e, "cd_backward_pointwise launch");
     return CD_OK;
 }

@@ -58,10 +58,12 @@ hipError_t launch_metrics(int64_t B, int64_t N, int64_t M, const float *dist_xy,
 
 // g_xy/g_yx per point when `pointwise`, else per item (grad_out) scaled by
 // sxy = w1/N and syx = w2/M.
+size_t backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
 hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
                            const float *g_yx, bool pointwise, float sxy, float syx,
                            const float *X, const float *Y, const int32_t *idx_xy,
-                           const int32_t *idx_yx, float *gX, float *gY, hipStream_t stream);
+                           const int32_t *idx_yx, float *gX, float *gY, void *ws,
+                           hipStream_t stream);
 
 // Backward of barycentric interpolation onto mesh vertices (bary_scatter.hip):
 // gV[v] = sum of w_{s,v} gP[s] (negated if `negate`) over the samples whose

@@ -11,7 +11,10 @@ Bars (per the readings in the design notes):
   * Chamfer within 1e-5 relative of the float64-accumulated oracle value;
   * F-score counts exact (same float32 distances, exact threshold test);
   * gradients within 1e-4 relative plus the float-atomic reordering bound
-    4 n 2^-24 S (n contributions with absolute sum S per component).
+    4 n 2^-24 S (n contributions with absolute sum S per component); since
+    the scatter sums are exact (fixed point), also within 4 2^-24 S + 2 2^-24
+    |g| (each term's float32 rounding plus one final rounding), and bitwise
+    equal from run to run.
 """
 from __future__ import annotations
 
@@ -109,6 +112,23 @@ def assert_grad(gX, gY, X, Y, idx_xy, idx_yx, grad_out, w1=1.0, w2=1.0, rel=1e-4
             raise AssertionError(f"{name} at {k}: gpu={g[k]} ref={r[k]} tol={tol[k]} n={n[k[:2]]}")
     return max(float(np.max(np.abs(gX - rX) / np.maximum(np.abs(rX), 1e-30))),
                float(np.max(np.abs(gY - rY) / np.maximum(np.abs(rY), 1e-30))))
+
+
+def assert_grad_exact_sums(gX, gY, X, Y, idx_xy, idx_yx, grad_out=None, w1=1.0, w2=1.0,
+                           g_xy=None, g_yx=None):
+    """The exact-sum bound: every term carries at most a few float32
+    roundings (difference, products, the per-item scale), the sum none, the
+    result one."""
+    if g_xy is None:
+        rX, rY, sX, sY, _, _ = oracle.backward(grad_out, X, Y, idx_xy, idx_yx, w1, w2)
+    else:
+        rX, rY, sX, sY, _, _ = oracle.backward_pointwise(g_xy, g_yx, X, Y, idx_xy, idx_yx)
+    for name, g, r, s in (("gX", gX, rX, sX), ("gY", gY, rY, sY)):
+        tol = 4 * U32 * s + 2 * U32 * np.abs(r) + 1e-38
+        err = np.abs(g.astype(np.float64) - r)
+        if not np.all(err <= tol):
+            k = np.unravel_index(np.argmax(err - tol), err.shape)
+            raise AssertionError(f"{name} at {k}: gpu={g[k]} ref={r[k]} tol={tol[k]}")
 
 
 def gradient_identities(gX, gY, X, Y, grad_out, chamfer_vals, rel=1e-4):

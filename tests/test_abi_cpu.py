@@ -115,12 +115,25 @@ def test_reduce_fscore_backward_reject_bad_args(lib):
         a = list(args)
         a[k] = None
         go, X, Y, ixy, iyx, gX, gY = a
-        assert lib.cd_backward(1, 3, 3, go, 1.0, 1.0, X, Y, ixy, iyx, gX, gY, None) == CD_ERR_INVALID_ARG
-    assert lib.cd_backward(-2, 3, 3, *([FAKE] * 1), 1.0, 1.0, *([FAKE] * 6), None) == CD_ERR_INVALID_ARG
+        assert lib.cd_backward(1, 3, 3, go, 1.0, 1.0, X, Y, ixy, iyx, gX, gY, FAKE, 1 << 30,
+                               None) == CD_ERR_INVALID_ARG
+    assert lib.cd_backward(-2, 3, 3, *([FAKE] * 1), 1.0, 1.0, *([FAKE] * 6), FAKE, 1 << 30,
+                           None) == CD_ERR_INVALID_ARG
     for k in range(8):
         a = [FAKE] * 8
         a[k] = None
-        assert lib.cd_backward_pointwise(1, 3, 3, *a, None) == CD_ERR_INVALID_ARG
+        assert lib.cd_backward_pointwise(1, 3, 3, *a, FAKE, 1 << 30, None) == CD_ERR_INVALID_ARG
+    need = lib.cd_backward_workspace_bytes(16, 16384, 16384)
+    assert need > 0 and need % 256 == 0
+    assert lib.cd_backward(16, 16384, 16384, *([FAKE] * 1), 1.0, 1.0, *([FAKE] * 6), FAKE,
+                           need - 1, None) == CD_ERR_WORKSPACE
+    assert lib.cd_backward_pointwise(4, 100000, 10000, *([FAKE] * 8), FAKE, 8,
+                                     None) == CD_ERR_WORKSPACE
+    assert lib.cd_backward_workspace_bytes(0, 3, 3) == 0
+    assert lib.cd_backward_workspace_bytes(2, 0, 3) == 0
+    # Bounded partials: a few hundred MB at most for the largest workloads.
+    for B, N, M in ((16, 16384, 16384), (4, 100000, 10000), (8, 65536, 65536), (1, 10 ** 6, 10 ** 6)):
+        assert lib.cd_backward_workspace_bytes(B, N, M) <= 400 << 20, (B, N, M)
 
 
 def test_metrics_rejects_bad_args(lib):

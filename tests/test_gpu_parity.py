@@ -112,6 +112,25 @@ def test_backward_pointwise_matches_oracle():
     for g, r, s, n in ((gc.to_np(gX), rX, sX, nX), (gc.to_np(gY), rY, sY, nY)):
         tol = 1e-4 * np.abs(r) + 4.0 * (n[..., None] + 2) * gc.U32 * s
         assert np.all(np.abs(g - r) <= tol)
+    gc.assert_grad_exact_sums(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx),
+                              g_xy=g_xy, g_yx=g_yx)
+
+
+@pytest.mark.parametrize("B,N,M", [(1, 300000, 700), (2, 5000, 90000), (3, 4096, 4097),
+                                   (1, 1, 50000), (5, 8193, 1)])
+def test_backward_chunked_senders_exact_and_reproducible(B, N, M):
+    """Shapes where one cloud's senders are split into several chunks (and
+    the other's are not): exact-sum bound against the oracle and bitwise
+    equal repeated runs; grid-quantised points give heavy contention."""
+    print(f"[case] backward B={B} N={N} M={M}", flush=True)
+    X, Y = synth.generate("grid_dup", B, N, M, 31 + N % 7)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    go = np.linspace(0.5, 1.5, B).astype(np.float32)
+    gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    gX2, gY2 = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    assert torch.equal(gX, gX2) and torch.equal(gY, gY2)
+    gc.assert_grad_exact_sums(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx), go)
 
 
 def test_autograd_chamfer_distance():
@@ -278,7 +297,11 @@ def test_full_size_workload(k):
         assert np.array_equal(gc.to_np(mf)[ti], gc.to_np(f))
     gXn, gYn = gc.to_np(gX), gc.to_np(gY)
     gc.assert_grad(gXn, gYn, X, Y, ixy_n, iyx_n, go)
+    gc.assert_grad_exact_sums(gXn, gYn, X, Y, ixy_n, iyx_n, go)
     gc.gradient_identities(gXn, gYn, X, Y, go, oracle.chamfer(dxy_n, dyx_n))
+    # Exact sums: the backward is bitwise reproducible.
+    gX2, gY2 = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    assert torch.equal(gX2, gX) and torch.equal(gY2, gY)
 
 
 @pytest.mark.parametrize("B,dims", [(16, (32, 32, 16)), (8, (64, 64, 16))],
