@@ -41,7 +41,9 @@ constexpr int kBlock = 512;                 // threads of a scatter workgroup
 constexpr int kSlice = 2048;                // receivers per workgroup
 constexpr int kUnroll = 8;                  // senders per thread per round
 constexpr int64_t kRound = static_cast<int64_t>(kBlock) * kUnroll;
-constexpr int kBoundBlock = 1024;           // points per bound block
+constexpr int kBoundThreads = 1024;
+constexpr int kBoundPer = 1;                // points of each cloud per thread
+constexpr int kBoundBlock = kBoundThreads * kBoundPer;   // points per bound block
 constexpr int kBound = 8;                   // per block: -min xyz, max xyz, max|g_xy|, max|g_yx|
 constexpr int kThreads = 256;
 
@@ -118,40 +120,57 @@ __device__ __forceinline__ float g2_recv(const Side &s, int64_t i)
 }
 
 template <bool kPointwise>
-__global__ __launch_bounds__(kBoundBlock) void bound_kernel(BwdArgs a)
+__global__ __launch_bounds__(kBoundThreads) void bound_kernel(BwdArgs a)
 {
-    __shared__ float red[kBoundBlock / kWave];
+    __shared__ float red[kBoundThreads / kWave][kBound];
     const int64_t b = blockIdx.x / a.nblk;
-    const int64_t blk = blockIdx.x % a.nblk;
-    const int64_t j = blk * kBoundBlock + threadIdx.x;
+    const int64_t j0 = (blockIdx.x % a.nblk) * static_cast<int64_t>(kBoundBlock) + threadIdx.x;
     // v[0..2] = -min, v[3..5] = max of the coordinates (so all are maxima).
     float v[kBound];
 #pragma unroll
-    for (int c = 0; c < kBound; ++c) v[c] = -__builtin_inff();
+    for (int c = 0; c < 6; ++c) v[c] = -__builtin_inff();
     v[6] = v[7] = 0.0f;
-    if (j < a.N) {
-        const float *x = a.X + (b * a.N + j) * 3;
-#pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            v[c] = fmaxf(v[c], -x[c]);
-            v[3 + c] = fmaxf(v[3 + c], x[c]);
-        }
-        v[6] = fabsf(kPointwise ? a.gxy[b * a.N + j] : a.gxy[b] * a.sxy);
+    if (!kPointwise) {
+        v[6] = fabsf(a.gxy[b] * a.sxy);
+        v[7] = fabsf(a.gyx[b] * a.syx);
     }
-    if (j < a.M) {
-        const float *y = a.Y + (b * a.M + j) * 3;
 #pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            v[c] = fmaxf(v[c], -y[c]);
-            v[3 + c] = fmaxf(v[3 + c], y[c]);
+    for (int u = 0; u < kBoundPer; ++u) {
+        const int64_t j = j0 + u * kBoundThreads;
+        if (j < a.N) {
+            const float *x = a.X + (b * a.N + j) * 3;
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                v[c] = fmaxf(v[c], -x[c]);
+                v[3 + c] = fmaxf(v[3 + c], x[c]);
+            }
+            if (kPointwise) v[6] = fmaxf(v[6], fabsf(a.gxy[b * a.N + j]));
         }
-        v[7] = fabsf(kPointwise ? a.gyx[b * a.M + j] : a.gyx[b] * a.syx);
+        if (j < a.M) {
+            const float *y = a.Y + (b * a.M + j) * 3;
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                v[c] = fmaxf(v[c], -y[c]);
+                v[3 + c] = fmaxf(v[3 + c], y[c]);
+            }
+            if (kPointwise) v[7] = fmaxf(v[7], fabsf(a.gyx[b * a.M + j]));
+        }
     }
-    float *out = a.bpart + (b * a.nblk + blk) * kBound;
 #pragma unroll
     for (int c = 0; c < kBound; ++c) {
-        const float m = group_max<kBoundBlock>(v[c], red);
-        if (threadIdx.x == 0) out[c] = m;
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) v[c] = fmaxf(v[c], __shfl_xor(v[c], off, kWave));
+    }
+    if (threadIdx.x % kWave == 0) {
+#pragma unroll
+        for (int c = 0; c < kBound; ++c) red[threadIdx.x / kWave][c] = v[c];
+    }
+    __syncthreads();
+    if (threadIdx.x < kBound) {
+        float m = red[0][threadIdx.x];
+#pragma unroll
+        for (int w = 1; w < kBoundThreads / kWave; ++w) m = fmaxf(m, red[w][threadIdx.x]);
+        a.bpart[blockIdx.x * kBound + threadIdx.x] = m;
     }
 }
 
@@ -368,10 +387,10 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
     const int64_t groups = B * (static_cast<int64_t>(p.ns[0]) * p.nc[0] +
                                 static_cast<int64_t>(p.ns[1]) * p.nc[1]);
     if (pointwise) {
-        bound_kernel<true><<<nbound, kBoundBlock, 0, stream>>>(a);
+        bound_kernel<true><<<nbound, kBoundThreads, 0, stream>>>(a);
         scatter_kernel<true><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
     } else {
-        bound_kernel<false><<<nbound, kBoundBlock, 0, stream>>>(a);
+        bound_kernel<false><<<nbound, kBoundThreads, 0, stream>>>(a);
         scatter_kernel<false><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
     }
     for (int s = 0; s < 2; ++s) {
