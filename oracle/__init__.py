@@ -18,6 +18,9 @@ Two independent implementations live here:
 * ``p2s_oracle.c``: the point-to-surface distance of Kaolin Sec. 2.5 (points
   to the closest face of a triangle mesh), its face choice and its backward
   to the points and vertices, in double.
+* ``emd_oracle`` (NumPy, float64): the approximate Earth-mover's distance of
+  Kaolin Sec. 2.5 as scheduled log-domain Sinkhorn iterations on the
+  Euclidean transport problem, and its fixed-plan backward.
 
 Every function follows Kaolin Sec. 2.5 (Chamfer distance for point clouds,
 defined through its citation of Fan et al.) under the readings listed in the
