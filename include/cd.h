@@ -268,6 +268,49 @@ cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const fl
                           const float *V, const int32_t *F, const int32_t *fidx, const float *g,
                           float *gP, float *gV, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Approximate Earth-mover's distance between point clouds (Kaolin Sec. 2.5:
+ * "a quadratic approximation of" EMD, by citation of Fan et al., whose EMD is
+ * the optimal transport cost with Euclidean ground distance).  Per item: the
+ * transport problem between X [B,N,3] and Y [B,M,3] with uniform masses 1/N,
+ * 1/M and cost C_ij = |x_i - y_j|, regularised by entropy and solved with
+ * log-domain Sinkhorn iterations (O(N M) work each).  Iteration t of
+ * n_iters uses eps_t = eps_start (eps_end / eps_start)^(t / (n_iters - 1))
+ * (eps_end if n_iters == 1) and updates
+ *   f_i <- -eps_t log sum_j (1/M) exp((g_j - C_ij) / eps_t), then
+ *   g_j <- -eps_t log sum_i (1/N) exp((f_i - C_ij) / eps_t).
+ * The reported cost is sum_ij P_ij C_ij with P_ij = exp((f_i + g_j - C_ij) /
+ * eps_end) / (N M).  Evaluated in float32 (hardware square roots and
+ * exponentials); partial sums of the cost in double.  Shapes and checks as for
+ * cd_forward; eps_start, eps_end > 0 and finite, n_iters >= 1, else
+ * CD_ERR_INVALID_ARG.
+ */
+
+/* Device workspace bytes for cd_emd_forward and cd_emd_backward (0 for B == 0
+ * or invalid sizes); one buffer serves both. */
+size_t cd_emd_workspace_bytes(int64_t B, int64_t N, int64_t M);
+
+/*
+ * f [B,N], g [B,M]: the potentials, in/out.  warm_start == 0: g starts at 0
+ * (f need not be initialised); otherwise the iterations start from the g
+ * passed in (f is overwritten by the first update).  cost [B] float32.
+ * ws: cd_emd_workspace_bytes(B, N, M) bytes, 256-byte aligned.
+ */
+cd_status cd_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                         float eps_start, float eps_end, int n_iters, int warm_start, float *f,
+                         float *g, float *cost, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward of sum_b grad_out[b] cost[b] with the plan of (f, g, eps) held
+ * fixed (eps: the eps_end of the forward):
+ *   gX[b,i] = grad_out[b] sum_j P_ij (x_i - y_j) / C_ij
+ *   gY[b,j] = grad_out[b] sum_i P_ij (y_j - x_i) / C_ij   (terms with C_ij = 0 are 0).
+ * gX, gY fully overwritten; ws as for cd_emd_forward.
+ */
+cd_status cd_emd_backward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                          const float *f, const float *g, float eps, const float *grad_out,
+                          float *gX, float *gY, void *ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -37,7 +37,7 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["schedule", "sinkhorn", "plan", "cost_matrix", "backward"]
+__all__ = ["schedule", "sinkhorn", "sinkhorn_step", "plan", "cost_matrix", "backward"]
 
 
 def schedule(eps_start: float, eps_end: float, n_iters: int) -> np.ndarray:
@@ -83,6 +83,21 @@ def sinkhorn(X, Y, eps_start: float, eps_end: float, n_iters: int):
         cost[b] = (P * C).sum()
         F[b], G[b] = f, g
     return cost, F, G
+
+
+def sinkhorn_step(X, Y, G, eps: float):
+    """One iteration (the f-update, then the g-update) from given potentials
+    G [B, M] at regularisation eps: (F_new [B, N], G_new [B, M])."""
+    X = np.asarray(X, np.float32)
+    Y = np.asarray(Y, np.float32)
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    F = np.empty((B, N))
+    Gn = np.empty((B, M))
+    for b in range(B):
+        C = cost_matrix(X[b], Y[b])
+        F[b] = -eps * _lse((np.asarray(G[b], np.float64)[None, :] - C) / eps - np.log(M), axis=1)
+        Gn[b] = -eps * _lse((F[b][:, None] - C) / eps - np.log(N), axis=0)
+    return F, Gn
 
 
 def plan(f, g, C, eps):

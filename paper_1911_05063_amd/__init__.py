@@ -17,6 +17,8 @@ Functions (names follow the C ABI):
                                     -> differentiable mesh surface sampling (Sec. 2.1)
   p2s_forward / p2s_backward / point_to_surface
                                     -> point-to-surface distance to triangle meshes (Sec. 2.5)
+  emd_forward / emd_backward / earth_movers_distance
+                                    -> approximate EMD (scheduled Sinkhorn, Sec. 2.5)
   sample_points(V, F, S)            -> P [B, S, 3], differentiable in V (autograd)
 """
 from __future__ import annotations
@@ -32,7 +34,8 @@ __all__ = [
     "f_score", "metrics", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
     "ChamferDistance", "forward_step", "mesh_sample_faces", "mesh_sample_points",
     "mesh_sample_backward", "MeshSample", "sample_points", "p2s_forward", "p2s_backward",
-    "PointToSurface", "point_to_surface",
+    "PointToSurface", "point_to_surface", "emd_forward", "emd_backward", "EarthMoversDistance",
+    "earth_movers_distance",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcd_hip.so")
@@ -90,6 +93,14 @@ def library() -> ctypes.CDLL:
     lib.cd_p2s_forward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.cd_p2s_backward.restype = st
     lib.cd_p2s_backward.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp,
+                                    ctypes.c_size_t, vp]
+    lib.cd_emd_workspace_bytes.restype = ctypes.c_size_t
+    lib.cd_emd_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.cd_emd_forward.restype = st
+    lib.cd_emd_forward.argtypes = [i64, i64, i64, vp, vp, f32, f32, ctypes.c_int, ctypes.c_int,
+                                   vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.cd_emd_backward.restype = st
+    lib.cd_emd_backward.argtypes = [i64, i64, i64, vp, vp, vp, vp, f32, vp, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.cd_backward_pointwise.restype = st
     lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -444,3 +455,70 @@ def point_to_surface(P, V, F):
     """Per-point squared distances [B, S] (autograd); the point-to-surface loss
     of Sec. 2.5 is their mean over the points."""
     return PointToSurface.apply(P, V, F)[0]
+
+
+# ---------------------------------------------------------------- approximate EMD
+
+def _emd_ws(B, N, M, device):
+    need = int(library().cd_emd_workspace_bytes(B, N, M))
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+
+def emd_forward(X, Y, eps_start: float = 0.5, eps_end: float = 0.01, n_iters: int = 50,
+                g_init: Optional[torch.Tensor] = None):
+    """(cost [B], f [B, N], g [B, M]): approximate EMD by scheduled log-domain
+    Sinkhorn iterations (the schedule and updates are documented in cd.h)."""
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    f = torch.empty((B, N), dtype=torch.float32, device=X.device)
+    if g_init is None:
+        g = torch.empty((B, M), dtype=torch.float32, device=X.device)
+    else:
+        g = _device_tensor(g_init, "g_init", torch.float32).clone()
+    cost = torch.empty(B, dtype=torch.float32, device=X.device)
+    ws = _emd_ws(B, N, M, X.device)
+    with torch.cuda.device(X.device):
+        _check(library().cd_emd_forward(B, N, M, _ptr(X), _ptr(Y), float(eps_start),
+                                        float(eps_end), int(n_iters), int(g_init is not None),
+                                        _ptr(f), _ptr(g), _ptr(cost), _ptr(ws), ws.numel(),
+                                        ctypes.c_void_p(_stream(X.device))), "cd_emd_forward")
+    return cost, f, g
+
+
+def emd_backward(X, Y, f, g, eps: float, grad_out):
+    """(gX, gY) of sum_b grad_out[b] cost[b] with the plan held fixed."""
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    f = _device_tensor(f, "f", torch.float32)
+    g = _device_tensor(g, "g", torch.float32)
+    go = _device_tensor(grad_out, "grad_out", torch.float32)
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    gX = torch.empty_like(X)
+    gY = torch.empty_like(Y)
+    ws = _emd_ws(B, N, M, X.device)
+    with torch.cuda.device(X.device):
+        _check(library().cd_emd_backward(B, N, M, _ptr(X), _ptr(Y), _ptr(f), _ptr(g), float(eps),
+                                         _ptr(go), _ptr(gX), _ptr(gY), _ptr(ws), ws.numel(),
+                                         ctypes.c_void_p(_stream(X.device))), "cd_emd_backward")
+    return gX, gY
+
+
+class EarthMoversDistance(torch.autograd.Function):
+    """Approximate EMD per item [B]; the backward holds the transport plan fixed."""
+
+    @staticmethod
+    def forward(ctx, X, Y, eps_start, eps_end, n_iters):
+        cost, f, g = emd_forward(X, Y, eps_start, eps_end, n_iters)
+        ctx.save_for_backward(X, Y, f, g)
+        ctx.eps = eps_end
+        return cost
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        X, Y, f, g = ctx.saved_tensors
+        gX, gY = emd_backward(X, Y, f, g, ctx.eps, grad_out.contiguous().float())
+        return gX, gY, None, None, None
+
+
+def earth_movers_distance(X, Y, eps_start: float = 0.5, eps_end: float = 0.01, n_iters: int = 50):
+    """Approximate EMD [B] between X [B, N, 3] and Y [B, M, 3] (autograd)."""
+    return EarthMoversDistance.apply(X, Y, eps_start, eps_end, n_iters)

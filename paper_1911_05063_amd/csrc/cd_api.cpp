@@ -348,4 +348,48 @@ cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const fl
     return CD_OK;
 }
 
+size_t cd_emd_workspace_bytes(int64_t B, int64_t N, int64_t M)
+{
+    if (check_shape(B, N, M) != CD_OK || B == 0) return 0;
+    return (cdk::emd_workspace_bytes(B, N, M) + 255) & ~static_cast<size_t>(255);
+}
+
+static bool positive_finite(float v) { return v > 0.0f && std::isfinite(v); }
+
+cd_status cd_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                         float eps_start, float eps_end, int n_iters, int warm_start, float *f,
+                         float *g, float *cost, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (!positive_finite(eps_start) || !positive_finite(eps_end))
+        return invalid("eps_start and eps_end must be positive and finite");
+    if (n_iters < 1) return invalid("n_iters < 1");
+    if (B == 0) return CD_OK;
+    if (!X || !Y || !f || !g || !cost) return invalid("NULL array pointer");
+    s = check_ws(cd_emd_workspace_bytes(B, N, M), ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e = cdk::launch_emd_forward(B, N, M, X, Y, eps_start, eps_end, n_iters,
+                                                 warm_start != 0, f, g, cost, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_emd_forward launch");
+    return CD_OK;
+}
+
+cd_status cd_emd_backward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                          const float *f, const float *g, float eps, const float *grad_out,
+                          float *gX, float *gY, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (!positive_finite(eps)) return invalid("eps must be positive and finite");
+    if (B == 0) return CD_OK;
+    if (!X || !Y || !f || !g || !grad_out || !gX || !gY) return invalid("NULL array pointer");
+    s = check_ws(cd_emd_workspace_bytes(B, N, M), ws, ws_bytes);
+    if (s != CD_OK) return s;
+    const hipError_t e =
+        cdk::launch_emd_backward(B, N, M, X, Y, f, g, eps, grad_out, gX, gY, ws, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_emd_backward launch");
+    return CD_OK;
+}
+
 }  // extern "C"

@@ -105,4 +105,14 @@ hipError_t launch_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, con
                                const float *V, const int32_t *F, const int32_t *fidx,
                                const float *g, float *gP, float *gV, void *ws, hipStream_t stream);
 
+// Approximate Earth-mover's distance (emd.hip): scheduled log-domain Sinkhorn.
+size_t emd_workspace_bytes(int64_t B, int64_t N, int64_t M);
+float emd_eps(double eps_start, double eps_end, int n_iters, int t);
+hipError_t launch_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                              double eps_start, double eps_end, int n_iters, bool warm, float *f,
+                              float *g, float *cost, void *ws, hipStream_t stream);
+hipError_t launch_emd_backward(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                               const float *f, const float *g, double eps, const float *go,
+                               float *gX, float *gY, void *ws, hipStream_t stream);
+
 }  // namespace cdk

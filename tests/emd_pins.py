@@ -141,6 +141,19 @@ def pin_fixed_plan_gradient(orc):
                 assert abs(fd - grad[i, c]) <= 1e-6 * (1 + abs(fd)), (i, c, fd, grad[i, c])
 
 
+def pin_step_composes_to_the_schedule(orc):
+    # The one-iteration function, applied along the schedule from g = 0,
+    # reproduces the scheduled run.
+    rng = np.random.default_rng(11)
+    X = rng.normal(0, 1, (2, 9, 3)).astype(np.float32)
+    Y = rng.normal(0, 1, (2, 13, 3)).astype(np.float32)
+    cost, F, G = orc.sinkhorn(X, Y, 0.7, 0.05, 7)
+    g = np.zeros((2, 13))
+    for e in orc.schedule(0.7, 0.05, 7):
+        f, g = orc.sinkhorn_step(X, Y, g, e)
+    assert np.allclose(f, F, rtol=0, atol=1e-12) and np.allclose(g, G, rtol=0, atol=1e-12)
+
+
 def pin_schedule(orc):
     s = orc.schedule(1.0, 0.01, 3)
     assert np.allclose(s, [1.0, 0.1, 0.01], rtol=1e-15, atol=0)
@@ -149,4 +162,4 @@ def pin_schedule(orc):
 
 ALL_PINS = [pin_hand_worked, pin_exact_assignment, pin_one_dimensional_sorted_matching,
             pin_marginals_unequal_sizes, pin_invariances, pin_identical_clouds,
-            pin_fixed_plan_gradient, pin_schedule]
+            pin_fixed_plan_gradient, pin_step_composes_to_the_schedule, pin_schedule]

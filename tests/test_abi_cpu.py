@@ -233,3 +233,24 @@ def test_p2s_entry_points_reject_bad_args(lib):
                                None) == CD_ERR_INVALID_ARG
     assert lib.cd_p2s_backward(1, 5, 3, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 8,
                                None) == CD_ERR_WORKSPACE
+
+
+def test_emd_entry_points_reject_bad_args(lib):
+    assert lib.cd_emd_workspace_bytes(2, 100, 50) > 0
+    assert lib.cd_emd_workspace_bytes(0, 100, 50) == 0
+    assert lib.cd_emd_workspace_bytes(2, 0, 50) == 0
+    ws = FAKE
+    ok_args = (FAKE, FAKE, 0.5, 0.01, 10, 0, FAKE, FAKE, FAKE, ws, 1 << 30, None)
+    assert lib.cd_emd_forward(1, 5, 5, FAKE, FAKE, 0.0, 0.01, 10, 0, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_forward(1, 5, 5, FAKE, FAKE, 0.5, float("nan"), 10, 0, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_forward(1, 5, 5, FAKE, FAKE, 0.5, 0.01, 0, 0, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_forward(1, 0, 5, *ok_args) == CD_ERR_INVALID_ARG
+    for k in (0, 1, 6, 7, 8):
+        a = list(ok_args)
+        a[k] = None
+        assert lib.cd_emd_forward(1, 5, 5, *a) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_forward(1, 5, 5, FAKE, FAKE, 0.5, 0.01, 10, 0, FAKE, FAKE, FAKE, ws, 8, None) == CD_ERR_WORKSPACE
+    assert lib.cd_emd_forward(0, 5, 5, None, None, 0.5, 0.01, 10, 0, None, None, None, None, 0, None) == CD_OK
+    assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, FAKE, -1.0, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, FAKE, FAKE, ws, 8, None) == CD_ERR_WORKSPACE

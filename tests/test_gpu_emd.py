@@ -1,0 +1,127 @@
+"""GPU parity of the approximate EMD (scheduled log-domain Sinkhorn, Kaolin
+Sec. 2.5) against the float64 oracle: one iteration from the same potentials
+(tight), a full scheduled run (errors add at most linearly: each update is
+non-expansive in the potentials' sup norm), the cost, and the fixed-plan
+backward."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+import gpu_checks as gc
+from oracle import emd_oracle
+
+pytestmark = pytest.mark.gpu
+U32 = 2.0 ** -24
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm GPU visible")
+    import paper_1911_05063_amd as cd
+    assert os.path.exists(cd.LIB_PATH), "libcd_hip.so missing: build before running GPU tests"
+    yield
+
+
+import paper_1911_05063_amd as cd  # noqa: E402
+
+
+def _cmax(X, Y):
+    lo = np.minimum(X.min(1), Y.min(1))
+    hi = np.maximum(X.max(1), Y.max(1))
+    return np.sqrt(((hi - lo).astype(np.float64) ** 2).sum(-1)).max()
+
+
+def _step_tol(eps, nt, cmax, pmax):
+    """Bound on one float32 half-update: distance and hardware square root
+    (2^-21 C), the exponent's rounding (2^-24 |z| eps ~ 2^-24 (C + |p|)), the
+    float32 running sum over nt terms and the hardware exp2/log2 (2^-21)."""
+    return 2.0 ** -20 * cmax + 2.0 ** -22 * pmax + eps * ((nt + 32) * U32 + 2.0 ** -20)
+
+
+@pytest.mark.parametrize("B,N,M,eps", [(2, 700, 1300, 0.05), (3, 1100, 513, 0.01), (1, 3000, 3000, 0.2),
+                                       (2, 1, 257, 0.05), (1, 4500, 90, 0.02)])
+def test_one_iteration_matches_oracle(B, N, M, eps):
+    print(f"[case] emd step B={B} N={N} M={M} eps={eps}", flush=True)
+    X, Y = synth.generate("sphere", B, N, M, 7 + N % 5)
+    # Realistic input potentials: a few oracle iterations.
+    _, _, G0 = emd_oracle.sinkhorn(X, Y, 0.5, eps, 4)
+    G0 = G0.astype(np.float32)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    cost, f, g = cd.emd_forward(Xg, Yg, eps, eps, 1, g_init=gc.to_gpu(G0))
+    f, g = gc.to_np(f), gc.to_np(g)
+    cmax = _cmax(X, Y)
+    F_or, _ = emd_oracle.sinkhorn_step(X, Y, G0, eps)
+    tol_f = _step_tol(eps, M, cmax, np.abs(G0).max())
+    assert np.max(np.abs(f - F_or)) <= tol_f, (np.max(np.abs(f - F_or)), tol_f)
+    # The g-update, from the GPU's own f (the swapped problem's first half-update).
+    G_or, _ = emd_oracle.sinkhorn_step(Y, X, f, eps)
+    tol_g = _step_tol(eps, N, cmax, np.abs(f).max())
+    assert np.max(np.abs(g - G_or)) <= tol_g, (np.max(np.abs(g - G_or)), tol_g)
+
+
+def test_full_schedule_cost_and_backward():
+    B, N, M, iters, e0, e1 = 2, 1500, 1200, 40, 0.5, 0.02
+    X, Y = synth.generate("sphere", B, N, M, 11)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    cost, f, g = cd.emd_forward(Xg, Yg, e0, e1, iters)
+    cost, f, g = gc.to_np(cost), gc.to_np(f), gc.to_np(g)
+    c_or, F_or, G_or = emd_oracle.sinkhorn(X, Y, e0, e1, iters)
+    cmax = _cmax(X, Y)
+    pmax = max(np.abs(F_or).max(), np.abs(G_or).max())
+    # Each update is non-expansive in the sup norm of the potentials, so the
+    # per-step errors add at most linearly over the 2 * iters updates.
+    delta = sum(_step_tol(e, max(N, M), cmax, pmax) for e in emd_oracle.schedule(e0, e1, iters)) * 2
+    assert np.max(np.abs(f - F_or)) <= delta and np.max(np.abs(g - G_or)) <= delta
+    # Cost: the plan's relative error is at most 2 delta / eps_end (both
+    # potentials), plus the float32 plan-pass products and sums.
+    tol_c = c_or * (2 * delta / e1 + (max(N, M) + 64) * U32)
+    assert np.all(np.abs(cost - c_or) <= tol_c), (cost, c_or, tol_c)
+    # Cost from the GPU's own potentials, in float64: tighter.
+    own = np.array([(emd_oracle.plan(f[b], g[b], emd_oracle.cost_matrix(X[b], Y[b]), e1)
+                     * emd_oracle.cost_matrix(X[b], Y[b])).sum() for b in range(B)])
+    assert np.all(np.abs(cost - own) <= own * (cmax / e1 * 2.0 ** -20 + (M + 64) * U32)), (cost, own)
+    # Backward with the plan of the GPU's potentials held fixed.
+    go = np.array([1.0, 0.5], np.float32)
+    gX, gY = cd.emd_backward(Xg, Yg, gc.to_gpu(f), gc.to_gpu(g), e1, gc.to_gpu(go))
+    rX, rY = emd_oracle.backward(X, Y, f.astype(np.float64), g.astype(np.float64), e1, go)
+    # Each term's weight carries a relative error of about (2^-21 C + 2^-23 |f + g|) / eps
+    # in the exponent plus 2^-20 from rsqrt / exp2; terms are bounded by the row mass.
+    rel = (2.0 ** -21 * cmax + 2.0 ** -23 * 2 * pmax) / e1 + 2.0 ** -19
+    tolX = go[:, None, None] * (rel / N + (M + 16) * U32 / N)
+    tolY = go[:, None, None] * (rel / M + (N + 16) * U32 / M)
+    assert np.all(np.abs(gc.to_np(gX) - rX) <= tolX), np.max(np.abs(gc.to_np(gX) - rX) - tolX)
+    assert np.all(np.abs(gc.to_np(gY) - rY) <= tolY), np.max(np.abs(gc.to_np(gY) - rY) - tolY)
+
+
+def test_autograd_and_degenerate_inputs():
+    X, Y = synth.generate("uniform", 2, 300, 200, 13)
+    Xg = gc.to_gpu(X).requires_grad_(True)
+    Yg = gc.to_gpu(Y).requires_grad_(True)
+    cost = cd.earth_movers_distance(Xg, Yg, 0.5, 0.05, 20)
+    cost.sum().backward()
+    assert torch.isfinite(Xg.grad).all() and torch.isfinite(Yg.grad).all()
+    # Translation invariance of the gradients' sum: sum gX + sum gY = 0.
+    tot = Xg.grad.double().sum(1) + Yg.grad.double().sum(1)
+    assert torch.all(tot.abs() < 1e-5), tot
+    # Identical clouds (zero distances on the diagonal) and a single point.
+    Z = gc.to_gpu(X[:, :50])
+    c, f, g = cd.emd_forward(Z, Z.clone(), 0.5, 0.01, 60)
+    gX, gY = cd.emd_backward(Z, Z, f, g, 0.01, torch.ones(2, device="cuda:0"))
+    assert torch.isfinite(c).all() and torch.isfinite(gX).all() and torch.isfinite(gY).all()
+    assert torch.all(c < 0.01 * 2 * np.log(50) + 1e-3), c
+    c1, _, _ = cd.emd_forward(gc.to_gpu(X[:, :1]), gc.to_gpu(Y[:, :1]), 0.5, 0.05, 3)
+    want = np.sqrt(((X[:, 0].astype(np.float64) - Y[:, 0]) ** 2).sum(-1))
+    assert np.allclose(gc.to_np(c1), want, rtol=1e-5), (c1, want)
+
+
+def test_reproducible():
+    X, Y = synth.generate("gmm", 2, 2000, 900, 17)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    a = cd.emd_forward(Xg, Yg, 0.5, 0.02, 10)
+    b = cd.emd_forward(Xg, Yg, 0.5, 0.02, 10)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
