@@ -44,12 +44,13 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=100,
                     help="untimed steps; the GPU clock ramps up during the first ~50 ms")
     ap.add_argument("--workload", type=int, default=3, help="workload number 1..5 (default 3)")
-    ap.add_argument("--path", choices=("chamfer", "mesh", "p2s"), default="chamfer",
+    ap.add_argument("--path", choices=("chamfer", "mesh", "p2s", "emd"), default="chamfer",
                     help="chamfer: the Chamfer step on the workload (default); mesh: the mesh "
                          "reconstruction loss step (surface sampling -> Chamfer -> vertex "
                          "gradients) on 16 meshes of 200 triangles, 16384 samples each; "
                          "p2s: the point-to-surface loss step on 16 deformed icospheres of "
-                         "5120 faces against 16384 points each")
+                         "5120 faces against 16384 points each; emd: the approximate EMD step "
+                         "(50 Sinkhorn iterations + backward) on the sphere workload")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
@@ -396,8 +397,115 @@ def p2s_step_bench(args):
     print(json.dumps(out), flush=True)
 
 
+# Sinkhorn half-update pair function (an FMA counts 2): the distance (3 sub,
+# 3 mul, 2 add), its square root (1), the exponent (fma: 2), the batch
+# maximum (1), the shifted exponent (sub 1, exp2 1) and the sum (1).
+EMD_FLOPS_PER_PAIR = 15
+EMD_ITERS, EMD_EPS = 50, (0.5, 0.01)
+
+
+def time_cpu_emd(X, Y, items):
+    """The oracle's scheduled Sinkhorn + backward on the first `items` items."""
+    import numpy as np
+    from oracle import emd_oracle
+    t0 = time.perf_counter()
+    cost, F, G = emd_oracle.sinkhorn(X[:items], Y[:items], EMD_EPS[0], EMD_EPS[1], EMD_ITERS)
+    emd_oracle.backward(X[:items], Y[:items], F, G, EMD_EPS[1], np.ones(items))
+    dt = time.perf_counter() - t0
+    pairs = float(items) * X.shape[1] * Y.shape[1] * (2 * EMD_ITERS + 3)
+    return {"value": pairs / dt, "unit": "Sinkhorn pair-evals/s", "cores": 1, "kind": "oracle",
+            "sample": f"{items} items x {X.shape[1]} x {Y.shape[1]} points, {EMD_ITERS} iterations "
+                      f"+ cost + backward (NumPy float64, dense cost matrix)"}
+
+
+def emd_step_bench(args):
+    """The approximate-EMD loss step (Sec. 2.5): cd_emd_forward (scheduled
+    Sinkhorn iterations and the transport cost) and cd_emd_backward."""
+    import numpy as np
+    import torch
+    import paper_1911_05063_amd as cd
+    import synth
+
+    w = synth.WORKLOADS[2]
+    X_np, Y_np = synth.workload(2)
+    B, N, M = w.B, w.N, w.M
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    X = torch.from_numpy(X_np).to(dev)
+    Y = torch.from_numpy(Y_np).to(dev)
+    lib = cd.library()
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    ws = torch.empty(int(lib.cd_emd_workspace_bytes(B, N, M)), dtype=torch.uint8, device=dev)
+    f = torch.empty((B, N), dtype=torch.float32, device=dev)
+    g = torch.empty((B, M), dtype=torch.float32, device=dev)
+    cost = torch.empty(B, dtype=torch.float32, device=dev)
+    go = torch.ones(B, dtype=torch.float32, device=dev)
+    gX, gY = torch.empty_like(X), torch.empty_like(Y)
+
+    def ok(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what}: {lib.cd_last_error().decode()}")
+
+    def one(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ok(lib.cd_emd_forward(B, N, M, ptr(X), ptr(Y), EMD_EPS[0], EMD_EPS[1], EMD_ITERS, 0,
+                              ptr(f), ptr(g), ptr(cost), ptr(ws), ws.numel(), st), "forward")
+        if ev is not None:
+            ev[1].record(stream)
+        ok(lib.cd_emd_backward(B, N, M, ptr(X), ptr(Y), ptr(f), ptr(g), EMD_EPS[1], ptr(go),
+                               ptr(gX), ptr(gY), ptr(ws), ws.numel(), st), "backward")
+        if ev is not None:
+            ev[2].record(stream)
+
+    print(f"[bench] emd on {w.describe()} iters={EMD_ITERS} eps={EMD_EPS} steps={args.steps} "
+          f"warmup={args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(args.steps):
+        one(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
+    bwd = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
+    pairs = float(B) * N * M * (2 * EMD_ITERS + 3)
+    lse_pairs = float(B) * N * M * 2 * EMD_ITERS
+    # The forward is dominated by the 2 * iters log-sum-exp passes; price them
+    # (the cost pass is a further B N M pairs inside the same interval).
+    achieved = EMD_FLOPS_PER_PAIR * lse_pairs / (fwd * 1e-3) / 1e12
+    out = {"metric": "approximate-EMD step Sinkhorn pair-evals/sec (50 iterations + cost + backward)",
+           "value": pairs / (ms * 1e-3), "unit": "Sinkhorn pair-evals/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "N": N, "M": M, "iters": EMD_ITERS,
+                      "eps": list(EMD_EPS)},
+           "ms_per_call": {"cd_emd_forward": fwd, "cd_emd_backward": bwd},
+           "roofline": {"bound": "alu", "kernel": "cd_emd_forward (lse passes + cost pass)",
+                        "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                        "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+                        "work_per_launch": f"{EMD_FLOPS_PER_PAIR} flop x {lse_pairs:.4g} "
+                                           f"log-sum-exp pair terms"}}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = time_cpu_emd(X_np, Y_np, 1)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse_args()
+    if args.path == "emd":
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        emd_step_bench(args)
+        return
     if args.path == "p2s":
         if args.gpus != 1:
             print("bench.py measures one GPU only", file=sys.stderr)

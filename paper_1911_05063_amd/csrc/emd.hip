@@ -36,7 +36,7 @@ constexpr int kEThreads = 256;              // 4 waves
 constexpr int kEGroup = kEQ * kEThreads;    // queries per workgroup
 constexpr int kEBatch = 16;                 // targets per online-LSE batch
 constexpr int kEMinTB = 64;                 // targets per block, at least
-constexpr int64_t kETargetTiles = 2048;
+constexpr int64_t kETargetTiles = 512;
 constexpr int kThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -58,6 +58,32 @@ __device__ __forceinline__ float dist2(float qx, float qy, float qz, float tx, f
     return __builtin_fmaf(dz, dz, __builtin_fmaf(dy, dy, dx * dx));
 }
 
+// One batch of kEBatch targets for kEQ queries: running max m and sum s.
+__device__ __forceinline__ void lse_batch(const float (&qx)[kEQ], const float (&qy)[kEQ],
+                                          const float (&qz)[kEQ], float (&m)[kEQ],
+                                          float (&s)[kEQ], const float (&tx)[kEBatch],
+                                          const float (&ty)[kEBatch], const float (&tz)[kEBatch],
+                                          const float (&tk)[kEBatch], float kk)
+{
+#pragma unroll
+    for (int k = 0; k < kEQ; ++k) {
+        float z[kEBatch];
+        float bm = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < kEBatch; ++u) {
+            const float c = __builtin_amdgcn_sqrtf(dist2(qx[k], qy[k], qz[k], tx[u], ty[u], tz[u]));
+            z[u] = __builtin_fmaf(-c, kk, tk[u]);
+            bm = __builtin_fmaxf(bm, z[u]);
+        }
+        const float mn = __builtin_fmaxf(m[k], bm);
+        float acc = s[k] * __builtin_amdgcn_exp2f(m[k] - mn);
+#pragma unroll
+        for (int u = 0; u < kEBatch; ++u) acc += __builtin_amdgcn_exp2f(z[u] - mn);
+        s[k] = acc;
+        m[k] = mn;
+    }
+}
+
 __global__ __launch_bounds__(kEThreads) void lse_kernel(LseArgs a)
 {
     const int64_t per_item = static_cast<int64_t>(a.nQG) * a.nTB;
@@ -76,37 +102,37 @@ __global__ __launch_bounds__(kEThreads) void lse_kernel(LseArgs a)
         m[k] = -__builtin_inff();
         s[k] = 0.0f;
     }
-    const int64_t j0 = static_cast<int64_t>(tb) * a.TB;
-    const int64_t j1 = std::min<int64_t>(j0 + a.TB, a.nt);
+    // Targets [j0, j1) of item b; 32-bit offsets within the item.
+    const int j0 = tb * a.TB;
+    const int j1 = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(j0) + a.TB, a.nt));
+    const int jfull = j0 + (j1 - j0) / kEBatch * kEBatch;
     const float *Tb = a.T + b * a.nt * 3;
     const float *pb = a.pt + b * a.nt;
-    for (int64_t jb = j0; jb < j1; jb += kEBatch) {
+    const float kk = a.k;
+    for (int jb = j0; jb < jfull; jb += kEBatch) {
+        // A full batch: contiguous wave-uniform loads, no per-target guards.
         float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
 #pragma unroll
         for (int u = 0; u < kEBatch; ++u) {
-            const int64_t j = std::min<int64_t>(jb + u, j1 - 1);
+            tx[u] = Tb[3 * (jb + u) + 0];
+            ty[u] = Tb[3 * (jb + u) + 1];
+            tz[u] = Tb[3 * (jb + u) + 2];
+            tk[u] = pb[jb + u] * kk;
+        }
+        lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
+    }
+    if (jfull < j1) {
+        // The tail: clamped loads, weight 0 past the end.
+        float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
+#pragma unroll
+        for (int u = 0; u < kEBatch; ++u) {
+            const int j = std::min(jfull + u, j1 - 1);
             tx[u] = Tb[3 * j + 0];
             ty[u] = Tb[3 * j + 1];
             tz[u] = Tb[3 * j + 2];
-            tk[u] = jb + u < j1 ? pb[j] * a.k : -__builtin_inff();   // past the end: weight 0
+            tk[u] = jfull + u < j1 ? pb[j] * kk : -__builtin_inff();
         }
-#pragma unroll
-        for (int k = 0; k < kEQ; ++k) {
-            float z[kEBatch];
-            float bm = -__builtin_inff();
-#pragma unroll
-            for (int u = 0; u < kEBatch; ++u) {
-                const float c = __builtin_amdgcn_sqrtf(dist2(qx[k], qy[k], qz[k], tx[u], ty[u], tz[u]));
-                z[u] = __builtin_fmaf(-c, a.k, tk[u]);
-                bm = __builtin_fmaxf(bm, z[u]);
-            }
-            const float mn = __builtin_fmaxf(m[k], bm);
-            float acc = s[k] * __builtin_amdgcn_exp2f(m[k] - mn);
-#pragma unroll
-            for (int u = 0; u < kEBatch; ++u) acc += __builtin_amdgcn_exp2f(z[u] - mn);
-            s[k] = acc;
-            m[k] = mn;
-        }
+        lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
     }
 #pragma unroll
     for (int k = 0; k < kEQ; ++k) {
@@ -151,10 +177,38 @@ struct PlanArgs {
     int64_t nq, nt;
     float k;                // log2(e) / eps
     float mass;             // a b = 1 / (nq nt)
-    int gradient;
     int nQG, nTB, TB;
 };
 
+template <bool kGrad>
+__device__ __forceinline__ void plan_batch(const float (&qx)[kEQ], const float (&qy)[kEQ],
+                                           const float (&qz)[kEQ], const float (&qk)[kEQ],
+                                           float (&acc)[kEQ], float (&gx)[kEQ], float (&gy)[kEQ],
+                                           float (&gz)[kEQ], const float (&tx)[kEBatch],
+                                           const float (&ty)[kEBatch], const float (&tz)[kEBatch],
+                                           const float (&tk)[kEBatch], float kk)
+{
+#pragma unroll
+    for (int u = 0; u < kEBatch; ++u) {
+#pragma unroll
+        for (int k = 0; k < kEQ; ++k) {
+            const float d2 = dist2(qx[k], qy[k], qz[k], tx[u], ty[u], tz[u]);
+            const float r = d2 > 0.0f ? __builtin_amdgcn_rsqf(d2) : 0.0f;
+            const float c = d2 * r;
+            const float w = __builtin_amdgcn_exp2f(__builtin_fmaf(-c, kk, qk[k] + tk[u]));
+            if (kGrad) {
+                const float wr = w * r;
+                gx[k] = __builtin_fmaf(wr, qx[k] - tx[u], gx[k]);
+                gy[k] = __builtin_fmaf(wr, qy[k] - ty[u], gy[k]);
+                gz[k] = __builtin_fmaf(wr, qz[k] - tz[u], gz[k]);
+            } else {
+                acc[k] = __builtin_fmaf(w, c, acc[k]);
+            }
+        }
+    }
+}
+
+template <bool kGrad>
 __global__ __launch_bounds__(kEThreads) void plan_kernel(PlanArgs a)
 {
     __shared__ double red[kEThreads / kWave];
@@ -176,30 +230,36 @@ __global__ __launch_bounds__(kEThreads) void plan_kernel(PlanArgs a)
         qk[k] = in ? a.pq[b * a.nq + qc] * a.k : -__builtin_inff();   // outside: weight 0
         acc[k] = gx[k] = gy[k] = gz[k] = 0.0f;
     }
-    const int64_t j0 = static_cast<int64_t>(tb) * a.TB;
-    const int64_t j1 = std::min<int64_t>(j0 + a.TB, a.nt);
+    const int j0 = tb * a.TB;
+    const int j1 = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(j0) + a.TB, a.nt));
+    const int jfull = j0 + (j1 - j0) / kEBatch * kEBatch;
     const float *Tb = a.T + b * a.nt * 3;
     const float *pb = a.pt + b * a.nt;
-    for (int64_t j = j0; j < j1; ++j) {
-        const float tx = Tb[3 * j + 0], ty = Tb[3 * j + 1], tz = Tb[3 * j + 2];
-        const float tk = pb[j] * a.k;
+    const float kk = a.k;
+    for (int jb = j0; jb < jfull; jb += kEBatch) {
+        float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
 #pragma unroll
-        for (int k = 0; k < kEQ; ++k) {
-            const float d2 = dist2(qx[k], qy[k], qz[k], tx, ty, tz);
-            const float r = d2 > 0.0f ? __builtin_amdgcn_rsqf(d2) : 0.0f;
-            const float c = d2 * r;
-            const float w = __builtin_amdgcn_exp2f(__builtin_fmaf(-c, a.k, qk[k] + tk));
-            if (a.gradient) {
-                const float wr = w * r;
-                gx[k] = __builtin_fmaf(wr, qx[k] - tx, gx[k]);
-                gy[k] = __builtin_fmaf(wr, qy[k] - ty, gy[k]);
-                gz[k] = __builtin_fmaf(wr, qz[k] - tz, gz[k]);
-            } else {
-                acc[k] = __builtin_fmaf(w, c, acc[k]);
-            }
+        for (int u = 0; u < kEBatch; ++u) {
+            tx[u] = Tb[3 * (jb + u) + 0];
+            ty[u] = Tb[3 * (jb + u) + 1];
+            tz[u] = Tb[3 * (jb + u) + 2];
+            tk[u] = pb[jb + u] * kk;
         }
+        plan_batch<kGrad>(qx, qy, qz, qk, acc, gx, gy, gz, tx, ty, tz, tk, kk);
     }
-    if (a.gradient) {
+    if (jfull < j1) {
+        float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
+#pragma unroll
+        for (int u = 0; u < kEBatch; ++u) {
+            const int j = std::min(jfull + u, j1 - 1);
+            tx[u] = Tb[3 * j + 0];
+            ty[u] = Tb[3 * j + 1];
+            tz[u] = Tb[3 * j + 2];
+            tk[u] = jfull + u < j1 ? pb[j] * kk : -__builtin_inff();
+        }
+        plan_batch<kGrad>(qx, qy, qz, qk, acc, gx, gy, gz, tx, ty, tz, tk, kk);
+    }
+    if (kGrad) {
         const float sc = a.mass * a.go[b];
 #pragma unroll
         for (int k = 0; k < kEQ; ++k) {
@@ -207,10 +267,10 @@ __global__ __launch_bounds__(kEThreads) void plan_kernel(PlanArgs a)
             if (q >= a.nq) continue;
             float *dst = a.nTB == 1 ? a.grad + (b * a.nq + q) * 3
                                     : a.grad_part + ((b * a.nTB + tb) * a.nq + q) * 3;
-            const float s = a.nTB == 1 ? sc : 1.0f;
-            dst[0] = s * gx[k];
-            dst[1] = s * gy[k];
-            dst[2] = s * gz[k];
+            const float sv = a.nTB == 1 ? sc : 1.0f;
+            dst[0] = sv * gx[k];
+            dst[1] = sv * gy[k];
+            dst[2] = sv * gz[k];
         }
         return;
     }
@@ -342,11 +402,14 @@ hipError_t plan_pass(int64_t B, const float *Q, int64_t nq, const float *T, int6
     a.nt = nt;
     a.k = kLog2e / eps;
     a.mass = static_cast<float>(1.0 / (static_cast<double>(nq) * static_cast<double>(nt)));
-    a.gradient = gradient ? 1 : 0;
     a.nQG = t.nQG;
     a.nTB = t.nTB;
     a.TB = t.TB;
-    plan_kernel<<<static_cast<uint32_t>(B * t.nQG * t.nTB), kEThreads, 0, stream>>>(a);
+    const uint32_t grid = static_cast<uint32_t>(B * t.nQG * t.nTB);
+    if (gradient)
+        plan_kernel<true><<<grid, kEThreads, 0, stream>>>(a);
+    else
+        plan_kernel<false><<<grid, kEThreads, 0, stream>>>(a);
     if (gradient && t.nTB > 1)
         grad_merge_kernel<<<static_cast<uint32_t>(ceil_div(B * nq * 3, kThreads)), kThreads, 0,
                             stream>>>(a, B);
