@@ -25,9 +25,10 @@
  *    means "enqueued"; results are valid once the stream has reached them.
  *  - Arguments are checked before anything is enqueued, without touching
  *    device memory: a NULL pointer (when B > 0), B < 0, N < 1, M < 1,
- *    N or M >= 2^31 (indices are int32), a negative or NaN tau, or an
- *    unaligned workspace returns CD_ERR_INVALID_ARG.  B == 0 is a no-op that
- *    returns CD_OK.
+ *    N or M >= 2^31 (indices are int32), B * (N + M) > 2^31 (one thread per
+ *    point must fit a launch), a negative or NaN tau, or an unaligned
+ *    workspace returns CD_ERR_INVALID_ARG.  B == 0 is a no-op that returns
+ *    CD_OK.
  *  - Inputs must be finite and their squared distances must not overflow;
  *    other inputs are undefined behaviour.  Outputs must not alias inputs.
  *  - A failed launch returns CD_ERR_HIP; cd_last_error() then holds the HIP
@@ -282,8 +283,8 @@ cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const fl
  * The reported cost is sum_ij P_ij C_ij with P_ij = exp((f_i + g_j - C_ij) /
  * eps_end) / (N M).  Evaluated in float32 (hardware square roots and
  * exponentials); partial sums of the cost in double.  Shapes and checks as for
- * cd_forward; eps_start, eps_end > 0 and finite, n_iters >= 1, else
- * CD_ERR_INVALID_ARG.
+ * cd_forward, plus 3 B max(N, M) < 2^32 - 2^20; eps_start, eps_end > 0 and
+ * finite, n_iters >= 1, else CD_ERR_INVALID_ARG.
  */
 
 /* Device workspace bytes for cd_emd_forward and cd_emd_backward (0 for B == 0

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -37,9 +38,10 @@ cd_status check_shape(int64_t B, int64_t N, int64_t M)
     if (N < 1) return invalid("N < 1 (nearest neighbour over an empty cloud is undefined)");
     if (M < 1) return invalid("M < 1 (nearest neighbour over an empty cloud is undefined)");
     if (N > kMaxPoints || M > kMaxPoints) return invalid("N or M >= 2^31 (indices are int32)");
-    // Flattened per-thread indices (backward) and work items must fit the launch grid.
-    if (B > 0 && (B > (int64_t(1) << 40) / (N + M)))
-        return invalid("B * (N + M) too large for one launch");
+    // One thread per point of both clouds (the forward's merge, the backward's
+    // passes) must fit a launch: at most 2^31 points in all.
+    if (B > 0 && B > (int64_t(1) << 31) / (N + M))
+        return invalid("B * (N + M) > 2^31 points for one launch");
     return CD_OK;
 }
 
@@ -365,6 +367,8 @@ cd_status cd_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, const 
     if (!positive_finite(eps_start) || !positive_finite(eps_end))
         return invalid("eps_start and eps_end must be positive and finite");
     if (n_iters < 1) return invalid("n_iters < 1");
+    if (B > 0 && 3 * B * std::max(N, M) > (int64_t(1) << 32) - (int64_t(1) << 20))
+        return invalid("3 B max(N, M) >= 2^32 (one thread per gradient component)");
     if (B == 0) return CD_OK;
     if (!X || !Y || !f || !g || !cost) return invalid("NULL array pointer");
     s = check_ws(cd_emd_workspace_bytes(B, N, M), ws, ws_bytes);
@@ -382,6 +386,8 @@ cd_status cd_emd_backward(int64_t B, int64_t N, int64_t M, const float *X, const
     cd_status s = check_shape(B, N, M);
     if (s != CD_OK) return s;
     if (!positive_finite(eps)) return invalid("eps must be positive and finite");
+    if (B > 0 && 3 * B * std::max(N, M) > (int64_t(1) << 32) - (int64_t(1) << 20))
+        return invalid("3 B max(N, M) >= 2^32 (one thread per gradient component)");
     if (B == 0) return CD_OK;
     if (!X || !Y || !f || !g || !grad_out || !gX || !gY) return invalid("NULL array pointer");
     s = check_ws(cd_emd_workspace_bytes(B, N, M), ws, ws_bytes);

@@ -254,3 +254,15 @@ def test_emd_entry_points_reject_bad_args(lib):
     assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, FAKE, -1.0, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
     assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, FAKE, ws, 1 << 30, None) == CD_ERR_INVALID_ARG
     assert lib.cd_emd_backward(1, 5, 5, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, FAKE, FAKE, ws, 8, None) == CD_ERR_WORKSPACE
+
+
+def test_launch_size_limits(lib):
+    # One thread per point of both clouds must fit a launch.
+    assert lib.cd_workspace_bytes(1, 2 ** 30, 2 ** 30) > 0
+    assert lib.cd_workspace_bytes(2, 2 ** 30, 2 ** 30) == 0
+    assert lib.cd_workspace_bytes(4, 2 ** 29, 2 ** 29 + 1) == 0
+    assert lib.cd_backward_workspace_bytes(2, 2 ** 30, 2 ** 30) == 0
+    assert lib.cd_forward(2, 2 ** 30, 2 ** 30, *([FAKE] * 6), FAKE, 1 << 40, None) == CD_ERR_INVALID_ARG
+    # The EMD gradient merge: one thread per component, 3 B max(N, M) < 2^32.
+    assert lib.cd_emd_forward(1, 2 ** 30 + 2 ** 29, 10, FAKE, FAKE, 0.5, 0.01, 1, 0, FAKE, FAKE, FAKE,
+                              FAKE, 1 << 40, None) == CD_ERR_INVALID_ARG
