@@ -15,8 +15,11 @@
 //    length.  A face with a vertex index out of range gets a record at which
 //    every distance overflows to +inf, so it is never chosen.
 //  * p2s_search_kernel: a workgroup holds 2048 points (8 per lane) in VGPRs
-//    and walks a block of faces; the face index is wave-uniform, so the
-//    records come in through scalar loads and serve as SGPR operands.  Per
+//    and walks a block of at most 320 faces, whose records it first copies
+//    to LDS; each face's record is then read by every lane from the same LDS
+//    address (a broadcast) into VGPRs, so the arithmetic has VGPR operands
+//    only, which this chip can issue two at a time (SGPR operands measured
+//    13% slower).  Per
 //    (point, face): v = p - a; if min(s, t, 1 - s - t) >= threshold the
 //    projection is inside and dist = (v.n)^2, else dist = the minimum over the
 //    three edges of |v - clamp(v.e/|e|^2, 0, 1) e|^2 (the closest point of a
@@ -46,6 +49,7 @@ constexpr int kPWaves = 4;
 constexpr int kPThreads = kPWaves * kWave;
 constexpr int kPGroup = kPQ * kPThreads;    // points per workgroup
 constexpr int kMinFB = 64;        // faces per block, at least
+constexpr int kMaxFB = 320;       // faces per block, at most (records staged in 40 KB of LDS)
 constexpr int64_t kTargetTiles = 2048;
 constexpr int kThreads = 256;
 
@@ -164,15 +168,23 @@ __global__ __launch_bounds__(kPThreads) void p2s_search_kernel(P2SArgs a)
     const int32_t f0 = fb * a.FB;
     const int32_t f1 = static_cast<int32_t>(std::min<int64_t>(f0 + a.FB, a.nf));
     const float *rb = a.rec + b * a.nf * kRec;
+    __shared__ float4 lrec[kMaxFB * (kRec / 4)];
+    {
+        const float4 *src4 = reinterpret_cast<const float4 *>(rb + static_cast<int64_t>(f0) * kRec);
+        const int n4 = (f1 - f0) * (kRec / 4);
+        for (int t = threadIdx.x; t < n4; t += kPThreads) lrec[t] = src4[t];
+    }
+    __syncthreads();
     for (int32_t f = f0; f < f1; ++f) {
-        const float *r = rb + static_cast<int64_t>(f) * kRec;
-        const float ax = r[0], ay = r[1], az = r[2];
-        const float g0x = r[3], g0y = r[4], g0z = r[5];
-        const float g1x = r[6], g1y = r[7], g1z = r[8];
-        const float nx = r[9], ny = r[10], nz = r[11], cin = r[12];
-        const float e0x = r[13], e0y = r[14], e0z = r[15], n0x = r[16], n0y = r[17], n0z = r[18];
-        const float e1x = r[19], e1y = r[20], e1z = r[21], n1x = r[22], n1y = r[23], n1z = r[24];
-        const float e2x = r[25], e2y = r[26], e2z = r[27], n2x = r[28], n2y = r[29], n2z = r[30];
+        const float4 *r4 = lrec + (f - f0) * (kRec / 4);
+        const float4 A0 = r4[0], A1 = r4[1], A2 = r4[2], A3 = r4[3], A4 = r4[4], A5 = r4[5], A6 = r4[6], A7 = r4[7];
+        const float ax = A0.x, ay = A0.y, az = A0.z;
+        const float g0x = A0.w, g0y = A1.x, g0z = A1.y;
+        const float g1x = A1.z, g1y = A1.w, g1z = A2.x;
+        const float nx = A2.y, ny = A2.z, nz = A2.w, cin = A3.x;
+        const float e0x = A3.y, e0y = A3.z, e0z = A3.w, n0x = A4.x, n0y = A4.y, n0z = A4.z;
+        const float e1x = A4.w, e1y = A5.x, e1z = A5.y, n1x = A5.z, n1y = A5.w, n1z = A6.x;
+        const float e2x = A6.y, e2y = A6.z, e2z = A6.w, n2x = A7.x, n2y = A7.y, n2z = A7.z;
 #pragma unroll
         for (int k = 0; k < kPQ; ++k) {
             const float vx = px[k] - ax, vy = py[k] - ay, vz = pz[k] - az;
@@ -327,6 +339,7 @@ P2SPlan plan_p2s(int64_t B, int64_t S, int64_t nf)
     const int64_t groups = B * p.nQG;
     int64_t want = groups > 0 ? ceil_div(kTargetTiles, groups) : 1;
     want = std::max<int64_t>(1, std::min(want, ceil_div(nf, kMinFB)));
+    want = std::max<int64_t>(want, ceil_div(nf, kMaxFB));
     p.FB = static_cast<int>(ceil_div(nf, want));
     p.nFB = static_cast<int>(ceil_div(nf, p.FB));
     return p;
