@@ -231,6 +231,11 @@ void search_kernel(KernelArgs a)
     for (int t = threadIdx.x; t < t1 - t0; t += kThreads) cp[t0 + t] = colkeys[t];
 }
 
+// One point's coordinates: 12-byte loads (dword-aligned vector loads).
+struct P3 {
+    float x, y, z;
+};
+
 // Thread per output point: threads [0, B*N) finish rows, the rest columns.
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
                                                               int32_t *ixy, float *dyx,
@@ -249,14 +254,13 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         int js = static_cast<int>(static_cast<uint32_t>(key));
         js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
         const int je = js + min(kBatch, a.M - js);
-        const float *x = a.X + 3 * t;
-        const float *Yb = a.Y + b * a.M * 3;
-        const float px = x[0], py = x[1], pz = x[2];
+        const P3 x = reinterpret_cast<const P3 *>(a.X)[t];
+        const P3 *Yb = reinterpret_cast<const P3 *>(a.Y + b * a.M * 3);
         int found = -1;
 #pragma unroll 8
         for (int jj = je - 1; jj >= js; --jj) {
-            const float *ty = Yb + 3 * static_cast<int64_t>(jj);
-            const float d = sq_dist(px, py, pz, ty[0], ty[1], ty[2]);
+            const P3 ty = Yb[jj];
+            const float d = sq_dist(x.x, x.y, x.z, ty.x, ty.y, ty.z);
             found = (d == val) ? jj : found;
         }
         dxy[t] = val;
@@ -269,14 +273,19 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
 #pragma unroll 8
         for (int q = 0; q < a.nQG; ++q) key = min(key, cp[static_cast<int64_t>(q) * a.M]);
         const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
+        // Candidates: the kQ x-points of the winning lane, as a fixed-length,
+        // fully unrolled scan (indices clamped to the last one) so that all
+        // loads are in flight together.
         const int64_t i0 = static_cast<int64_t>(static_cast<uint32_t>(key)) * kQ;
-        const int64_t i1 = min(i0 + kQ, a.N);
-        const float *y = a.Y + 3 * u;
-        const float *Xb = a.X + b * a.N * 3;
-        const float px = y[0], py = y[1], pz = y[2];
+        const int64_t il = min(i0 + kQ, static_cast<int64_t>(a.N)) - 1;
+        const P3 y = reinterpret_cast<const P3 *>(a.Y)[u];
+        const P3 *Xb = reinterpret_cast<const P3 *>(a.X + b * a.N * 3);
         int64_t found = -1;
-        for (int64_t ii = i1 - 1; ii >= i0; --ii) {
-            const float d = sq_dist(Xb[3 * ii], Xb[3 * ii + 1], Xb[3 * ii + 2], px, py, pz);
+#pragma unroll
+        for (int k = kQ - 1; k >= 0; --k) {
+            const int64_t ii = min(i0 + k, il);
+            const P3 tx = Xb[ii];
+            const float d = sq_dist(tx.x, tx.y, tx.z, y.x, y.y, y.z);
             found = (d == val) ? ii : found;
         }
         dyx[u] = val;
