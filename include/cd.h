@@ -145,10 +145,12 @@ size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
  *   ws: cd_backward_workspace_bytes(B, N, M) bytes, 256-byte aligned
  *   (CD_ERR_WORKSPACE if smaller).
  * Each term is evaluated in float32; the scatter sums are exact: every term is
- * rounded to a 64-bit fixed-point integer (grid 2^-k, k per item and cloud
- * from the largest term, about 2^-61 * (cloud size) times it) and the
- * integers are added, so the result is bitwise reproducible run to run; own
- * term + sum are added in double and rounded once.  A point whose index lies
+ * rounded to a 64-bit fixed-point integer (grid 2^-k, with k from a bound on
+ * the largest term: per block of 2048 receivers when the other cloud has at
+ * most 16384 points, else per item and cloud; the grid is about 2^-61 times
+ * the number of terms times that bound) and the integers are added, so the
+ * result is bitwise reproducible run to run; own term + sum are added in
+ * double and rounded once.  A point whose index lies
  * outside [0, M) / [0, N) contributes nothing (its own and scatter terms are
  * dropped).
  */

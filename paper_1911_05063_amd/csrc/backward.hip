@@ -10,19 +10,25 @@
 //
 // The scatter sums are exact and therefore bitwise reproducible: every
 // contribution (a float32 product) is rounded to a 64-bit fixed-point integer
-// and the integers are added, so their order does not matter.
-//  * bound_kernel: per block of 1024 points of an item, the bounding box of
-//    both clouds and the largest |dL/d dist|.  Every contribution component
-//    is at most 2 |g| times the box's largest extent, which gives the
-//    fixed-point shift (fixed_point.h) keeping every receiver's sum below
-//    2^62; the grid is then about 2^-61 * (cloud size) * 2 |g| * extent,
-//    far below float32 rounding of the terms.  Coalesced reads, no gathers.
+// on a grid 2^-k and the integers are added, so their order does not matter.
+// k keeps every receiver's sum below 2^62 (fixed_point.h), from a bound on
+// the largest term:
+//  * "local" sides (senders fit one pass and one chunk): the largest term the
+//    workgroup itself queued, so k is per slice of receivers and needs no
+//    extra pass; the grid is about 2^-61 * (terms queued) * (largest term).
+//  * other sides: bound_kernel's per-item bound, shared by all chunks: per
+//    block of 1024 points of an item, the bounding box of both clouds and the
+//    largest |dL/d dist|; every term component is at most 2 |g| times the
+//    box's largest extent; the grid is about 2^-61 * (cloud size) times that.
+// Either grid is far below the float32 rounding of the terms.
 //  * scatter_kernel: a workgroup owns a slice of 2048 receivers of one cloud
-//    and item and a chunk of the other cloud's senders; it scans the chunk's
-//    neighbour indices (8 per thread per round, every load issued before the
-//    first wait) and adds the terms that land in its slice to LDS int64
-//    accumulators (ds_add_u64).  With one chunk per item it then writes
-//    own + scatter directly; otherwise the slice goes to the workspace.
+//    and item and a chunk of the other cloud's senders.  Per pass of 16384
+//    senders it loads their neighbour indices (32 per thread, all in flight
+//    at once), queues the senders that land in its slice in LDS (a wave
+//    prefix sum and one LDS atomic per wave), and then evaluates only the
+//    queued terms, adding them to LDS int64 accumulators (ds_add_u64).  With
+//    one chunk per item it then writes own + scatter directly (the own terms
+//    are loaded at the start); otherwise the slice goes to the workspace.
 //  * finalize_kernel: per receiver, the chunks' integer partials summed
 //    exactly, scaled back, plus the own term (in double), rounded once.
 // Senders are split into chunks only on a side whose scan is much longer than
@@ -38,9 +44,15 @@ namespace cdk {
 namespace {
 
 constexpr int kBlock = 512;                 // threads of a scatter workgroup
-constexpr int kSlice = 2048;                // receivers per workgroup
-constexpr int kUnroll = 8;                  // senders per thread per round
-constexpr int64_t kRound = static_cast<int64_t>(kBlock) * kUnroll;
+constexpr int kSliceBits = 11;
+constexpr int kSlice = 1 << kSliceBits;     // receivers per workgroup
+constexpr int kIdx = 32;                    // sender indices per thread per pass
+constexpr int64_t kPass = static_cast<int64_t>(kBlock) * kIdx;   // senders per pass
+constexpr int kOwn = kSlice / kBlock;       // receivers per thread (own terms, output)
+constexpr int kHold = 8;                    // queued terms per thread kept in registers
+constexpr uint32_t kXcds = 8;               // accelerator complex dies of an MI355X
+static_assert(kSlice % kBlock == 0, "receivers must divide evenly among the threads");
+static_assert((kPass << kSliceBits) <= (int64_t{1} << 32), "queue entry must fit 32 bits");
 constexpr int kBoundThreads = 1024;
 constexpr int kBoundPer = 1;                // points of each cloud per thread
 constexpr int kBoundBlock = kBoundThreads * kBoundPer;   // points per bound block
@@ -64,7 +76,8 @@ struct BwdArgs {
     int nblk;           // bound blocks per item (of the larger cloud)
     int ns[2];          // receiving slices per item (side 0: X receives, 1: Y)
     int nc[2];          // sender chunks per item
-    int64_t chunk[2];   // senders per chunk (a multiple of kRound)
+    int local[2];       // shift from the workgroup's own terms (one chunk, one pass)
+    int64_t chunk[2];   // senders per chunk (a multiple of kPass)
     int64_t poff[2];    // first partial of each side in part
 };
 
@@ -174,30 +187,89 @@ __global__ __launch_bounds__(kBoundThreads) void bound_kernel(BwdArgs a)
     }
 }
 
-// Own term of receiver p plus the scatter sum (double), rounded once.
+// Own term 2 g(r) (r - s) of receiver p, s its own neighbour (0 if that
+// index is outside the sender cloud).
 template <bool kPointwise>
-__device__ __forceinline__ void write_point(const BwdArgs &a, const Side &s, int side, int64_t b,
-                                            int64_t p, const double scat[3])
+__device__ __forceinline__ void own_term(const Side &s, int64_t p, float own[3])
 {
     const int32_t nb = s.ridx[p];
     const bool ok = nb >= 0 && nb < s.n_send;
     const int64_t qn = ok ? nb : 0;
     const float g2 = ok ? g2_recv<kPointwise>(s, p) : 0.0f;
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
-        const float own = g2 * (s.R[3 * p + c] - s.S[3 * qn + c]);
-        s.out[3 * p + c] = static_cast<float>(static_cast<double>(own) + scat[c]);
+    for (int c = 0; c < 3; ++c) own[c] = g2 * (s.R[3 * p + c] - s.S[3 * qn + c]);
+}
+
+// Own term plus the scatter sum (double), rounded once.
+__device__ __forceinline__ void write_point(const Side &s, int64_t p, const float own[3],
+                                            const double scat[3])
+{
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+        s.out[3 * p + c] = static_cast<float>(static_cast<double>(own[c]) + scat[c]);
+}
+
+// Term -2 g(s) (s - r) of queue entry e (sender offset from `base` in the
+// high bits, receiver offset from r0 in the low kSliceBits); ir = receiver
+// offset.
+template <bool kPointwise>
+__device__ __forceinline__ void queued_term(const Side &s, int64_t base, int64_t r0, uint32_t e,
+                                            float t[3], int &ir)
+{
+    const int64_t q = base + (e >> kSliceBits);
+    ir = static_cast<int>(e & (kSlice - 1));
+    const int64_t i = r0 + ir;
+    const float g2 = g2_send<kPointwise>(s, q);
+#pragma unroll
+    for (int d = 0; d < 3; ++d) t[d] = -(g2 * (s.S[3 * q + d] - s.R[3 * i + d]));
+}
+
+__device__ __forceinline__ void add_term(unsigned long long *acc, int ir, const float t[3], int ks)
+{
+#pragma unroll
+    for (int d = 0; d < 3; ++d)
+        atomicAdd(acc + 3 * ir + d, static_cast<unsigned long long>(to_fixed(t[d], ks)));
+}
+
+__device__ __forceinline__ float max_abs3(float m, const float t[3])
+{
+    return fmaxf(m, fmaxf(fabsf(t[0]), fmaxf(fabsf(t[1]), fabsf(t[2]))));
+}
+
+// Exclusive prefix sum of v over the wave (lane order) and the wave's total.
+__device__ __forceinline__ int wave_prefix(int v, int &total)
+{
+    const int lane = threadIdx.x % kWave;
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int n = __shfl_up(incl, off, kWave);
+        incl += lane >= off ? n : 0;
     }
+    total = __shfl(incl, kWave - 1, kWave);
+    return incl - v;
 }
 
 template <bool kPointwise>
 __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
 {
     __shared__ unsigned long long acc[3 * kSlice];
+    __shared__ uint32_t queue[kPass];
     __shared__ float red[kBlock / kWave];
+    __shared__ uint32_t qcount;
+    const int tid = threadIdx.x;
+    // Workgroups go to the XCDs round-robin.  With one sender chunk per side,
+    // the slices of one item and side read the same sender indices and
+    // coordinates, so consecutive groups are placed on one XCD (one L2);
+    // chunked shapes keep the plain order, which spreads the heavier side.
+    uint32_t wg = blockIdx.x;
+    if (a.nc[0] == 1 && a.nc[1] == 1) {
+        const uint32_t per = gridDim.x / kXcds;
+        if (wg < kXcds * per) wg = (wg % kXcds) * per + wg / kXcds;
+    }
     const int64_t g0 = a.B * a.ns[0] * a.nc[0];
-    const int side = blockIdx.x < g0 ? 0 : 1;
-    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int side = wg < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? wg : wg - g0;
     const int ns = a.ns[side], nc = a.nc[side];
     const int64_t b = g / (static_cast<int64_t>(ns) * nc);
     const int rest = static_cast<int>(g % (static_cast<int64_t>(ns) * nc));
@@ -205,79 +277,126 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
     const Side s = side_of<kPointwise>(a, side, b);
     const int64_t r0 = static_cast<int64_t>(slice) * kSlice;
     const int64_t r1 = std::min<int64_t>(r0 + kSlice, s.n_recv);
+    const bool local = a.local[side] != 0;
 
-    // The shift: every contribution component is at most 2 max|g_send| times
-    // the largest extent of the item's bounding box.
-    const float *bp = a.bpart + b * a.nblk * kBound;
-    float v[kBound];
+    // Own terms of this thread's receivers (with one chunk; otherwise the
+    // finalize pass adds them): independent of the scatter, so loaded first.
+    float own[kOwn][3];
+    if (nc == 1) {
 #pragma unroll
-    for (int c = 0; c < kBound; ++c) v[c] = -__builtin_inff();
-    for (int64_t k = threadIdx.x; k < a.nblk; k += kBlock) {
-#pragma unroll
-        for (int c = 0; c < kBound; ++c) v[c] = fmaxf(v[c], bp[k * kBound + c]);
+        for (int k = 0; k < kOwn; ++k)
+            own_term<kPointwise>(s, std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1), own[k]);
     }
-    float ext = 0.0f;
-#pragma unroll
-    for (int c = 0; c < 3; ++c) ext = fmaxf(ext, v[3 + c] + v[c]);      // max - min
-    const float gs = side == 0 ? v[7] : v[6];                            // senders' |g|
-    const float m = 2.0f * gs * ext;
-    const int ks = fixed_shift(group_max<kBlock>(m, red), s.n_send);
-    if (slice == 0 && c == 0 && threadIdx.x == 0) a.shift[b * 2 + side] = ks;
 
-    for (int t = threadIdx.x; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
+    for (int t = tid; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
+    if (tid == 0) qcount = 0u;
+    int ks = 0;
+    if (!local) {
+        // Every term component is at most 2 max|g_send| times the largest
+        // extent of the item's bounding box.
+        const float *bp = a.bpart + b * a.nblk * kBound;
+        float v[kBound];
+#pragma unroll
+        for (int k = 0; k < kBound; ++k) v[k] = -__builtin_inff();
+        for (int64_t k = tid; k < a.nblk; k += kBlock) {
+#pragma unroll
+            for (int u = 0; u < kBound; ++u) v[u] = fmaxf(v[u], bp[k * kBound + u]);
+        }
+        float ext = 0.0f;
+#pragma unroll
+        for (int d = 0; d < 3; ++d) ext = fmaxf(ext, v[3 + d] + v[d]);   // max - min
+        const float gs = side == 0 ? v[7] : v[6];                         // senders' |g|
+        ks = fixed_shift(group_max<kBlock>(2.0f * gs * ext, red), s.n_send);
+        if (slice == 0 && c == 0 && tid == 0) a.shift[b * 2 + side] = ks;
+    }
     __syncthreads();
 
-    // Scatter terms of this chunk's senders whose neighbour lies in the slice:
-    // -2 g(s) (s - r) added to r.  Out-of-slice lanes read a clamped, valid
-    // address and add nothing.
     const int64_t q0 = c * a.chunk[side];
     const int64_t q1 = std::min<int64_t>(q0 + a.chunk[side], s.n_send);
-    for (int64_t base = q0; base < q1; base += kRound) {
-        int64_t qs[kUnroll], is[kUnroll];
-        bool in[kUnroll];
+    for (int64_t base = q0; base < q1; base += kPass) {
+        // The pass's neighbour indices, all loads in flight together; queue
+        // the senders whose neighbour lies in the slice.
+        int32_t iv[kIdx];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int64_t q = base + static_cast<int64_t>(u) * kBlock + threadIdx.x;
-            qs[u] = std::min<int64_t>(q, q1 - 1);
-            const int64_t i = s.sidx[qs[u]];
-            in[u] = q < q1 && i >= r0 && i < r1;
-            is[u] = in[u] ? i : r0;
+        for (int u = 0; u < kIdx; ++u) {
+            const int64_t q = base + static_cast<int64_t>(u) * kBlock + tid;
+            iv[u] = q < q1 ? s.sidx[q] : -1;
         }
-        float sv[kUnroll][3], rv[kUnroll][3], g2[kUnroll];
+        int cnt = 0;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kIdx; ++u) cnt += (iv[u] >= r0 && iv[u] < r1) ? 1 : 0;
+        int total;
+        const int excl = wave_prefix(cnt, total);
+        uint32_t wbase = 0u;
+        if (tid % kWave == 0 && total > 0) wbase = atomicAdd(&qcount, static_cast<uint32_t>(total));
+        uint32_t pos = static_cast<uint32_t>(__shfl(static_cast<int>(wbase), 0, kWave) + excl);
 #pragma unroll
-            for (int d = 0; d < 3; ++d) {
-                sv[u][d] = s.S[3 * qs[u] + d];
-                rv[u][d] = s.R[3 * is[u] + d];
+        for (int u = 0; u < kIdx; ++u) {
+            if (iv[u] >= r0 && iv[u] < r1)
+                queue[pos++] = (static_cast<uint32_t>(u * kBlock + tid) << kSliceBits) |
+                               static_cast<uint32_t>(iv[u] - r0);
+        }
+        __syncthreads();
+        const int qlen = static_cast<int>(qcount);
+
+        if (local) {
+            // The only pass: the shift comes from the largest queued term.
+            float hold[kHold][3];
+            int hir[kHold];
+            float m = 0.0f;
+#pragma unroll
+            for (int h = 0; h < kHold; ++h) {
+                const int e = tid + h * kBlock;
+                if (e < qlen) {
+                    queued_term<kPointwise>(s, base, r0, queue[e], hold[h], hir[h]);
+                    m = max_abs3(m, hold[h]);
+                }
             }
-            g2[u] = g2_send<kPointwise>(s, qs[u]);
-        }
+            for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
+                float t[3];
+                int ir;
+                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
+                m = max_abs3(m, t);
+            }
+            ks = fixed_shift(group_max<kBlock>(m, red), qlen);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            if (in[u]) {
-                unsigned long long *t = acc + 3 * (is[u] - r0);
-#pragma unroll
-                for (int d = 0; d < 3; ++d)
-                    atomicAdd(t + d, static_cast<unsigned long long>(
-                                         to_fixed(-(g2[u] * (sv[u][d] - rv[u][d])), ks)));
+            for (int h = 0; h < kHold; ++h)
+                if (tid + h * kBlock < qlen) add_term(acc, hir[h], hold[h], ks);
+            for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
+                float t[3];
+                int ir;
+                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
+                add_term(acc, ir, t, ks);
+            }
+        } else {
+            for (int e = tid; e < qlen; e += kBlock) {
+                float t[3];
+                int ir;
+                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
+                add_term(acc, ir, t, ks);
             }
         }
+        __syncthreads();
+        if (tid == 0) qcount = 0u;
+        __syncthreads();
     }
-    __syncthreads();
 
     if (nc == 1) {
-        for (int64_t p = r0 + threadIdx.x; p < r1; p += kBlock) {
-            const unsigned long long *t = acc + 3 * (p - r0);
-            const double scat[3] = {ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
-                                    ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
-                                    ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
-            write_point<kPointwise>(a, s, side, b, p, scat);
+#pragma unroll
+        for (int k = 0; k < kOwn; ++k) {
+            const int64_t p = r0 + tid + k * kBlock;
+            if (p < r1) {
+                const unsigned long long *t = acc + 3 * (p - r0);
+                const double scat[3] = {
+                    ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
+                    ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
+                    ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
+                write_point(s, p, own[k], scat);
+            }
         }
     } else {
         long long *dst = a.part + a.poff[side] + ((b * nc + c) * s.n_recv + r0) * 3;
-        for (int t = threadIdx.x; t < 3 * (r1 - r0); t += kBlock)
-            dst[t] = static_cast<long long>(acc[t]);
+        for (int t = tid; t < 3 * (r1 - r0); t += kBlock) dst[t] = static_cast<long long>(acc[t]);
     }
 }
 
@@ -303,7 +422,9 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(BwdArgs a, int side)
     const double scat[3] = {ldexp(static_cast<double>(static_cast<long long>(sum[0])), -ks),
                             ldexp(static_cast<double>(static_cast<long long>(sum[1])), -ks),
                             ldexp(static_cast<double>(static_cast<long long>(sum[2])), -ks)};
-    write_point<kPointwise>(a, s, side, b, p, scat);
+    float own[3];
+    own_term<kPointwise>(s, p, own);
+    write_point(s, p, own, scat);
 }
 
 int64_t ceil_div(int64_t x, int64_t y) { return (x + y - 1) / y; }
@@ -312,7 +433,8 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct BwdPlan {
     int nblk;
-    int ns[2], nc[2];
+    int ns[2], nc[2], local[2];
+    bool need_bound;
     int64_t chunk[2];
     size_t bpart_bytes, shift_bytes, part_elems[2];
 };
@@ -325,18 +447,20 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
     int64_t rounds[2];
     for (int s = 0; s < 2; ++s) {
         p.ns[s] = static_cast<int>(ceil_div(n_recv[s], kSlice));
-        rounds[s] = ceil_div(n_send[s], kRound);
+        rounds[s] = ceil_div(n_send[s], kPass);
     }
-    // A side whose workgroups would scan many more rounds than the other's
-    // splits its senders into chunks of about the other's length (at least 2
-    // rounds): the long scan is what bounds the kernel's time otherwise.
-    const int64_t target = std::max<int64_t>(2, std::min(rounds[0], rounds[1]));
+    // A side whose workgroups would scan many more passes than the other's
+    // splits its senders into chunks of about the other's length: the long
+    // scan is what bounds the kernel's time otherwise.
+    const int64_t target = std::min(rounds[0], rounds[1]);
     for (int s = 0; s < 2; ++s) {
         const int64_t want = ceil_div(rounds[s], target);
-        p.chunk[s] = ceil_div(rounds[s], want) * kRound;
+        p.chunk[s] = ceil_div(rounds[s], want) * kPass;
         p.nc[s] = static_cast<int>(ceil_div(n_send[s], p.chunk[s]));
+        p.local[s] = p.nc[s] == 1 && n_send[s] <= kPass;
         p.part_elems[s] = p.nc[s] > 1 ? static_cast<size_t>(B * p.nc[s] * n_recv[s] * 3) : 0;
     }
+    p.need_bound = !(p.local[0] && p.local[1]);
     p.bpart_bytes = align256(static_cast<size_t>(B * p.nblk) * kBound * 4);
     p.shift_bytes = align256(static_cast<size_t>(B * 2) * 4);
     return p;
@@ -379,6 +503,7 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
     for (int s = 0; s < 2; ++s) {
         a.ns[s] = p.ns[s];
         a.nc[s] = p.nc[s];
+        a.local[s] = p.local[s];
         a.chunk[s] = p.chunk[s];
     }
     a.poff[0] = 0;
@@ -387,10 +512,10 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
     const int64_t groups = B * (static_cast<int64_t>(p.ns[0]) * p.nc[0] +
                                 static_cast<int64_t>(p.ns[1]) * p.nc[1]);
     if (pointwise) {
-        bound_kernel<true><<<nbound, kBoundThreads, 0, stream>>>(a);
+        if (p.need_bound) bound_kernel<true><<<nbound, kBoundThreads, 0, stream>>>(a);
         scatter_kernel<true><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
     } else {
-        bound_kernel<false><<<nbound, kBoundThreads, 0, stream>>>(a);
+        if (p.need_bound) bound_kernel<false><<<nbound, kBoundThreads, 0, stream>>>(a);
         scatter_kernel<false><<<static_cast<uint32_t>(groups), kBlock, 0, stream>>>(a);
     }
     for (int s = 0; s < 2; ++s) {

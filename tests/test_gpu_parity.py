@@ -133,6 +133,43 @@ def test_backward_chunked_senders_exact_and_reproducible(B, N, M):
     gc.assert_grad_exact_sums(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx), go)
 
 
+def _concentrated(B, N, M, seed):
+    """X uniform; Y crowded around three points of X (so most of Y's
+    neighbour indices land on a few receivers of one slice)."""
+    rng = np.random.default_rng(seed)
+    X = rng.uniform(-1, 1, (B, N, 3)).astype(np.float32)
+    hubs = X[:, [3, 4, N - 1], :]
+    pick = rng.integers(0, 3, (B, M))
+    Y = np.take_along_axis(hubs, pick[..., None].repeat(3, -1), axis=1)
+    Y = (Y + rng.normal(0, 1e-3, (B, M, 3))).astype(np.float32)
+    return X, Y
+
+
+@pytest.mark.parametrize("B,N,M,kind", [(2, 3000, 16000, "hubs"), (1, 20000, 16384, "hubs"),
+                                        (1, 16384, 16385, "grid_dup"),
+                                        (1, 16385, 16384, "grid_dup")])
+def test_backward_concentrated_and_boundary_senders(B, N, M, kind):
+    """Many senders on a few receivers (more queued terms per workgroup than
+    it keeps in registers), and clouds on either side of the 16384-sender
+    limit of the per-slice shift: exact-sum bound and bitwise repeats, for
+    per-item and per-point dL/d dist."""
+    print(f"[case] backward {kind} B={B} N={N} M={M}", flush=True)
+    X, Y = _concentrated(B, N, M, 61) if kind == "hubs" else synth.generate(kind, B, N, M, 62)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    go = np.linspace(0.5, 1.5, B).astype(np.float32)
+    gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    gX2, gY2 = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx)
+    assert torch.equal(gX, gX2) and torch.equal(gY, gY2)
+    gc.assert_grad_exact_sums(gc.to_np(gX), gc.to_np(gY), X, Y, gc.to_np(ixy), gc.to_np(iyx), go)
+    rng = np.random.default_rng(63)
+    g_xy = rng.normal(0, 1, (B, N)).astype(np.float32)
+    g_yx = rng.normal(0, 1, (B, M)).astype(np.float32)
+    pX, pY = cd.chamfer_backward_pointwise(gc.to_gpu(g_xy), gc.to_gpu(g_yx), Xg, Yg, ixy, iyx)
+    gc.assert_grad_exact_sums(gc.to_np(pX), gc.to_np(pY), X, Y, gc.to_np(ixy), gc.to_np(iyx),
+                              g_xy=g_xy, g_yx=g_yx)
+
+
 def test_autograd_chamfer_distance():
     X, Y = synth.generate("mesh", 3, 700, 900, 31)
     Xg = gc.to_gpu(X).requires_grad_(True)
