@@ -34,7 +34,8 @@ if ROOT not in sys.path:
 METRIC = "Chamfer fwd+bwd pair-evals/sec and ms/call at B=16, N=M=16384; % FP32 VALU peak"
 PEAK_FP32_TFLOPS = 157.3          # MI355X FP32 vector, 256 CU x 2.4 GHz x 256 flop/clk
 FLOPS_PER_PAIR = 9                # 3 sub + 3 mul + 2 add + 1 min per directed pair-eval
-FORWARD_SOURCES = ("paper_1911_05063_amd/csrc/nn_search.hip",)  # kernels of cd_forward
+# Sources of cd_forward's kernels and the flags they are built with.
+FORWARD_SOURCES = ("paper_1911_05063_amd/csrc/nn_search.hip", "paper_1911_05063_amd/build.py")
 
 
 def parse_args():
