@@ -132,6 +132,30 @@ def traffic_record(kernel_sources):
     return rec
 
 
+def timed_steps(one, n_marks, steps, warmup, stream):
+    """Warm-up, then exactly `steps` timed steps between two synchronizations.
+
+    one(ev) runs a step and records the n_marks events of `ev` (None: no
+    events).  Every event is created before the warm-up, so the timed steps
+    follow the warm-up's synchronization without an idle gap: after a few
+    milliseconds idle the GPU clock drops and needs tens of calls to ramp
+    back up.  Returns (per-step events, total ms, wall seconds)."""
+    import torch
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_marks)] for _ in range(steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(warmup):
+        one(None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for k in range(steps):
+        one(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    return evs, start.elapsed_time(stop), time.perf_counter() - t0
+
+
 class Step:
     """Preallocated buffers and the C-ABI calls of one step (marshalling only)."""
 
@@ -264,17 +288,8 @@ def mesh_step_bench(args):
         if ev is not None:
             ev[3].record(stream)
 
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for k in range(args.steps):
-        one(evs[k])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    evs, total_ms, _ = timed_steps(one, 4, args.steps, args.warmup, stream)
+    ms = total_ms / args.steps
     samp = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
     cham = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
     sbwd = statistics.mean(e[2].elapsed_time(e[3]) for e in evs)
@@ -365,17 +380,8 @@ def p2s_step_bench(args):
 
     print(f"[bench] {w.name}: B={B} S={S} nv={nv} nf={nf} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for k in range(args.steps):
-        one(evs[k])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    evs, total_ms, _ = timed_steps(one, 3, args.steps, args.warmup, stream)
+    ms = total_ms / args.steps
     fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
     rest = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
     pairs = float(B) * S * nf
@@ -463,17 +469,8 @@ def emd_step_bench(args):
 
     print(f"[bench] emd on {w.describe()} iters={EMD_ITERS} eps={EMD_EPS} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for k in range(args.steps):
-        one(evs[k])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    evs, total_ms, _ = timed_steps(one, 3, args.steps, args.warmup, stream)
+    ms = total_ms / args.steps
     fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
     bwd = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
     pairs = float(B) * N * M * (2 * EMD_ITERS + 3)
@@ -553,22 +550,7 @@ def main():
         if ev is not None:
             ev[3].record(step.stream)
 
-    for _ in range(args.warmup):
-        one_step()
-    torch.cuda.synchronize()
-
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record(step.stream)
-    for k in range(args.steps):
-        one_step(evs[k])
-    stop.record(step.stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = start.elapsed_time(stop)
+    evs, total_ms, wall = timed_steps(one_step, 4, args.steps, args.warmup, step.stream)
     fwd = [e[0].elapsed_time(e[1]) for e in evs]
     red = [e[1].elapsed_time(e[2]) for e in evs]
     bwd = [e[2].elapsed_time(e[3]) for e in evs]
