@@ -18,7 +18,9 @@ struct FwdPlan {
     int32_t N, M;
     int32_t nQG;   // query groups per item
     int32_t nTB;   // target blocks per item
-    int32_t TB;    // targets per block (a multiple of the batch length)
+    int32_t TB;    // targets per large block (a multiple of the batch length)
+    int32_t nBig;  // large blocks per item; the nTB - nBig others hold TS targets
+    int32_t TS;    // targets per small block (a multiple of the batch length)
 };
 
 struct FwdArgs {

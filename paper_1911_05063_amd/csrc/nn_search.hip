@@ -23,6 +23,9 @@
 //    lane holding the minimum is found.  The 4 waves combine through a 64-bit
 //    LDS atomicMin on (distance bits << 32 | lane), which orders by distance
 //    then lane because distances are >= +0.
+//  * Target blocks: TB targets (256..512), except the last ones of every
+//    group, which are small (128) and sit at the end of the grid, so that the
+//    final round of workgroups is filled with short tiles.
 //  * Each tile writes one packed (distance, batch start) key per x-point and
 //    one (distance, lane) key per y-point to the workspace; a merge kernel
 //    takes the minimum key over tiles and recovers the exact lowest index by
@@ -43,6 +46,9 @@ constexpr int kLdsRow = kWave + 4;  // padded LDS row (floats) of the column tra
 constexpr int kMaxTB = 512;         // targets per block at most (LDS column keys)
 constexpr int kMinTB = 256;         // targets per block at least
 constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (4 rounds of 4 per CU on MI355X)
+constexpr int64_t kSlots = 256 * 4;     // workgroups resident at once: 256 CUs x 4
+constexpr int kSmallTB = 128;           // targets per block of the final, small tiles
+constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of at most this many rounds
 constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
@@ -80,6 +86,7 @@ struct KernelArgs {
     unsigned long long *rowpart;  // [B, nTB, N]  (distance, batch start) per x-point and block
     unsigned long long *colpart;  // [B, nQG, M]  (distance, x lane) per y-point and group
     int32_t N, M, nQG, nTB, TB;
+    int32_t TS, nBig;   // small blocks of TS targets follow nBig blocks of TB
     int32_t pad;
     int64_t B;
 };
@@ -185,13 +192,26 @@ void search_kernel(KernelArgs a)
     __shared__ __attribute__((aligned(16))) float ldsbuf[kWaves][kBatch * kLdsRow];
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
-    // blockIdx.x = (b * nQG + qg) * nTB + tb
-    const uint32_t tb = blockIdx.x % static_cast<uint32_t>(a.nTB);
-    const uint32_t rest = blockIdx.x / static_cast<uint32_t>(a.nTB);
+    // The grid holds every (item, group) tile of the nBig large blocks first,
+    // blockIdx.x = (b * nQG + qg) * nBig + tb, then those of the small blocks,
+    // which the dispatcher hands out last and so fill the final round.
+    const uint32_t nbig = static_cast<uint32_t>(a.nBig);
+    const uint32_t big_tiles = static_cast<uint32_t>(a.B) * a.nQG * nbig;
+    uint32_t tb, rest;
+    if (blockIdx.x < big_tiles) {
+        tb = blockIdx.x % nbig;
+        rest = blockIdx.x / nbig;
+    } else {
+        const uint32_t k = blockIdx.x - big_tiles, nsmall = static_cast<uint32_t>(a.nTB) - nbig;
+        tb = nbig + k % nsmall;
+        rest = k / nsmall;
+    }
     const uint32_t qg = rest % static_cast<uint32_t>(a.nQG);
     const uint32_t b = rest / static_cast<uint32_t>(a.nQG);
-    const int t0 = static_cast<int>(tb) * a.TB;
-    const int t1 = t0 + min(a.TB, a.M - t0);
+    const bool large = tb < nbig;
+    const int t0 = large ? static_cast<int>(tb) * a.TB
+                         : a.nBig * a.TB + static_cast<int>(tb - nbig) * a.TS;
+    const int t1 = t0 + min(large ? a.TB : a.TS, a.M - t0);
     const float *Xb = a.X + static_cast<int64_t>(b) * a.N * 3;
     const float *Yb = a.Y + static_cast<int64_t>(b) * a.M * 3;
 
@@ -326,7 +346,23 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
     int64_t TB = ceil_div(ceil_div(M, want_blocks), kBatch) * kBatch;
     TB = std::min<int64_t>(std::max<int64_t>(TB, kMinTB), kMaxTB);
     p.TB = static_cast<int32_t>(TB);
-    p.nTB = static_cast<int32_t>(ceil_div(M, TB));
+    p.TS = kSmallTB;
+    const int64_t blocks = ceil_div(M, TB);
+    if (groups * blocks <= kSmallRounds * kSlots) {
+        // A launch of a few rounds: the last targets of every group go to small
+        // blocks, about a quarter round of resident workgroups' worth of work.
+        // Dispatched last, they even out the end of the launch (tiles of one
+        // size finish unevenly and leave CUs idle while the final ones run).
+        const int64_t small = std::min<int64_t>(
+            M, ceil_div(ceil_div(kSlots / 4 * TB, groups), kSmallTB) * kSmallTB);
+        p.nBig = static_cast<int32_t>((M - small) / TB);
+        p.nTB = p.nBig +
+                static_cast<int32_t>(ceil_div(M - static_cast<int64_t>(p.nBig) * TB, kSmallTB));
+    } else {
+        // Many rounds: the end matters little, the extra row keys more.
+        p.nBig = static_cast<int32_t>(blocks);
+        p.nTB = p.nBig;
+    }
     return p;
 }
 
@@ -347,6 +383,8 @@ hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream
     a.nQG = p.nQG;
     a.nTB = p.nTB;
     a.TB = p.TB;
+    a.TS = p.TS;
+    a.nBig = p.nBig;
     a.pad = 0;
     a.B = p.B;
     search_kernel<<<static_cast<uint32_t>(forward_tiles(p)), kThreads, 0, stream>>>(a);
