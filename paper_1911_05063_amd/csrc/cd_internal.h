@@ -96,7 +96,9 @@ hipError_t launch_mesh_sample_backward(int64_t B, int64_t nv, int64_t nf, const 
 struct P2SPlan {
     int nQG;   // point groups per item
     int nFB;   // face blocks per item
-    int FB;    // faces per block
+    int FB;    // faces per large block
+    int nBig;  // large blocks per item; the nFB - nBig others hold FS faces
+    int FS;    // faces per small block
 };
 P2SPlan plan_p2s(int64_t B, int64_t S, int64_t nf);
 size_t p2s_workspace_bytes(int64_t B, int64_t S, int64_t nv, int64_t nf);

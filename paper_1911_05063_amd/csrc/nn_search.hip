@@ -48,7 +48,7 @@ constexpr int kMinTB = 256;         // targets per block at least
 constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (4 rounds of 4 per CU on MI355X)
 constexpr int64_t kSlots = 256 * 4;     // workgroups resident at once: 256 CUs x 4
 constexpr int kSmallTB = 128;           // targets per block of the final, small tiles
-constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of at most this many rounds
+constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of 1 to 8 rounds
 constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
@@ -348,9 +348,10 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
     p.TB = static_cast<int32_t>(TB);
     p.TS = kSmallTB;
     const int64_t blocks = ceil_div(M, TB);
-    if (groups * blocks <= kSmallRounds * kSlots) {
-        // A launch of a few rounds: the last targets of every group go to small
-        // blocks, about a quarter round of resident workgroups' worth of work.
+    if (groups * blocks >= kSlots && groups * blocks <= kSmallRounds * kSlots) {
+        // A launch of one to a few rounds: the last targets of every group go
+        // to small blocks, about a quarter round of resident workgroups' worth
+        // of work.
         // Dispatched last, they even out the end of the launch (tiles of one
         // size finish unevenly and leave CUs idle while the final ones run).
         const int64_t small = std::min<int64_t>(
@@ -359,7 +360,8 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
         p.nTB = p.nBig +
                 static_cast<int32_t>(ceil_div(M - static_cast<int64_t>(p.nBig) * TB, kSmallTB));
     } else {
-        // Many rounds: the end matters little, the extra row keys more.
+        // Less than a round (every tile runs at once) or many rounds (the end
+        // matters little, the extra row keys more): one block size.
         p.nBig = static_cast<int32_t>(blocks);
         p.nTB = p.nBig;
     }

@@ -51,6 +51,8 @@ constexpr int kPGroup = kPQ * kPThreads;    // points per workgroup
 constexpr int kMinFB = 64;        // faces per block, at least
 constexpr int kMaxFB = 320;       // faces per block, at most (records staged in 40 KB of LDS)
 constexpr int64_t kTargetTiles = 2048;
+constexpr int64_t kSlots = 256 * 4;   // workgroups resident at once: 256 CUs x 4
+constexpr int64_t kSmallRounds = 8;   // small face blocks only for launches of 1 to 8 rounds
 constexpr int kThreads = 256;
 
 struct P2SArgs {
@@ -61,6 +63,8 @@ struct P2SArgs {
     int32_t *fidx;       // [B, S]
     int64_t S, nf;
     int nQG, nFB, FB;
+    int nBig, FS;        // small blocks of FS faces follow nBig blocks of FB
+    int64_t B;
 };
 
 __global__ __launch_bounds__(kThreads) void face_record_kernel(int64_t B, int64_t nv, int64_t nf,
@@ -146,10 +150,22 @@ __device__ __forceinline__ float seg2(float vx, float vy, float vz, float ex, fl
 
 __global__ __launch_bounds__(kPThreads) void p2s_search_kernel(P2SArgs a)
 {
-    const int64_t tiles_per_item = static_cast<int64_t>(a.nQG) * a.nFB;
-    const int64_t b = blockIdx.x / tiles_per_item;
-    const int rest = static_cast<int>(blockIdx.x % tiles_per_item);
-    const int qg = rest / a.nFB, fb = rest % a.nFB;
+    // Every (item, group) tile of the nBig large face blocks first, then those
+    // of the small blocks, which the dispatcher hands out last.
+    const uint32_t nbig = static_cast<uint32_t>(a.nBig);
+    const uint32_t big_tiles = static_cast<uint32_t>(a.B * a.nQG) * nbig;
+    uint32_t fbu, rest;
+    if (blockIdx.x < big_tiles) {
+        fbu = blockIdx.x % nbig;
+        rest = blockIdx.x / nbig;
+    } else {
+        const uint32_t k = blockIdx.x - big_tiles, nsmall = static_cast<uint32_t>(a.nFB) - nbig;
+        fbu = nbig + k % nsmall;
+        rest = k / nsmall;
+    }
+    const int fb = static_cast<int>(fbu);
+    const int qg = static_cast<int>(rest % static_cast<uint32_t>(a.nQG));
+    const int64_t b = rest / static_cast<uint32_t>(a.nQG);
     const int64_t q0 = static_cast<int64_t>(qg) * kPGroup;
 
     float px[kPQ], py[kPQ], pz[kPQ], best[kPQ];
@@ -165,8 +181,9 @@ __global__ __launch_bounds__(kPThreads) void p2s_search_kernel(P2SArgs a)
         best[k] = __builtin_inff();
         bidx[k] = -1;
     }
-    const int32_t f0 = fb * a.FB;
-    const int32_t f1 = static_cast<int32_t>(std::min<int64_t>(f0 + a.FB, a.nf));
+    const bool large = fb < a.nBig;
+    const int32_t f0 = large ? fb * a.FB : a.nBig * a.FB + (fb - a.nBig) * a.FS;
+    const int32_t f1 = static_cast<int32_t>(std::min<int64_t>(f0 + (large ? a.FB : a.FS), a.nf));
     const float *rb = a.rec + b * a.nf * kRec;
     __shared__ float4 lrec[kMaxFB * (kRec / 4)];
     {
@@ -341,7 +358,21 @@ P2SPlan plan_p2s(int64_t B, int64_t S, int64_t nf)
     want = std::max<int64_t>(1, std::min(want, ceil_div(nf, kMinFB)));
     want = std::max<int64_t>(want, ceil_div(nf, kMaxFB));
     p.FB = static_cast<int>(ceil_div(nf, want));
-    p.nFB = static_cast<int>(ceil_div(nf, p.FB));
+    const int64_t blocks = ceil_div(nf, p.FB);
+    p.FS = std::max(1, p.FB / 4);
+    if (groups * blocks >= kSlots && groups * blocks <= kSmallRounds * kSlots) {
+        // A launch of one to a few rounds: the last faces of every item go to
+        // small blocks (a quarter of the size), about a quarter round of
+        // resident workgroups' worth of work, dispatched last to even out the
+        // end.
+        const int64_t small = std::min<int64_t>(
+            nf, ceil_div(ceil_div(kSlots / 4 * p.FB, std::max<int64_t>(groups, 1)), p.FS) * p.FS);
+        p.nBig = static_cast<int>((nf - small) / p.FB);
+        p.nFB = p.nBig + static_cast<int>(ceil_div(nf - static_cast<int64_t>(p.nBig) * p.FB, p.FS));
+    } else {
+        p.nBig = static_cast<int>(blocks);
+        p.nFB = p.nBig;
+    }
     return p;
 }
 
@@ -365,7 +396,7 @@ hipError_t launch_p2s_forward(int64_t B, int64_t S, int64_t nv, int64_t nf, cons
     uint64_t *part = reinterpret_cast<uint64_t *>(base + align256(static_cast<size_t>(B * nf) * kRec * 4));
     face_record_kernel<<<static_cast<uint32_t>(ceil_div(B * nf, kThreads)), kThreads, 0, stream>>>(
         B, nv, nf, V, F, rec);
-    P2SArgs a{P, rec, part, dist, fidx, S, nf, p.nQG, p.nFB, p.FB};
+    P2SArgs a{P, rec, part, dist, fidx, S, nf, p.nQG, p.nFB, p.FB, p.nBig, p.FS, B};
     p2s_search_kernel<<<static_cast<uint32_t>(B * p.nQG * p.nFB), kPThreads, 0, stream>>>(a);
     if (p.nFB > 1)
         p2s_merge_kernel<<<static_cast<uint32_t>(ceil_div(B * S, kThreads)), kThreads, 0, stream>>>(

@@ -47,8 +47,8 @@ SMALL_CASES = [
     ("gmm", 1, 6000, 90, 11),
     ("sphere", 5, 200, 4500, 12),
     # Large target blocks followed by small ones (and the boundary between
-    # them) on a tie-heavy cloud: 145 blocks of 256 targets, then 257 of 128.
-    ("grid_dup", 1, 3000, 70000, 13),
+    # them) on a tie-heavy cloud.
+    ("grid_dup", 2, 2100, 70000, 13),
 ]
 
 
