@@ -256,37 +256,81 @@ struct P3 {
     float x, y, z;
 };
 
-// Thread per output point: threads [0, B*N) finish rows, the rest columns.
+// Threads of the merge that finish rows: B*N rounded up to whole waves.
+__host__ __device__ __forceinline__ int64_t merge_row_threads(int64_t nx)
+{
+    return (nx + kWave - 1) / kWave * kWave;
+}
+
+// Rows first (threads [0, merge_row_threads(B*N))), then one thread per
+// column.  A wave of rows takes the minimum key of its 64 x-points (one per
+// lane), then rescans their candidate batches 8 x-points at a time: 8 lanes
+// per x-point, each lane 4 consecutive targets (48 contiguous bytes), and the
+// lowest matching index over the 8 lanes.
+
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
                                                               int32_t *ixy, float *dyx,
                                                               int32_t *iyx)
 {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * kMergeThreads + threadIdx.x;
     const int64_t nx = a.B * a.N;
-    if (t >= nx + a.B * a.M) return;
-    if (t < nx) {
-        const int64_t b = t / a.N, i = t - b * a.N;
-        const unsigned long long *rp = a.rowpart + b * a.nTB * static_cast<int64_t>(a.N) + i;
-        unsigned long long key = ~0ull;
+    const int64_t nr = merge_row_threads(nx);
+    if (t >= nr + a.B * a.M) return;
+    if (t < nr) {
+        // t < nr: whole waves, so every lane of this wave takes this branch.
+        const int lane = threadIdx.x % kWave;
+        const bool mine = t < nx;
+        float val = 0.0f, px = 0.0f, py = 0.0f, pz = 0.0f;
+        int js = a.M;
+        if (mine) {
+            const int64_t b = t / a.N, i = t - b * a.N;
+            const unsigned long long *rp = a.rowpart + b * a.nTB * static_cast<int64_t>(a.N) + i;
+            unsigned long long key = ~0ull;
 #pragma unroll 8
-        for (int tb = 0; tb < a.nTB; ++tb) key = min(key, rp[static_cast<int64_t>(tb) * a.N]);
-        const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
-        int js = static_cast<int>(static_cast<uint32_t>(key));
-        js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
-        const int je = js + min(kBatch, a.M - js);
-        const P3 x = reinterpret_cast<const P3 *>(a.X)[t];
-        const P3 *Yb = reinterpret_cast<const P3 *>(a.Y + b * a.M * 3);
-        int found = -1;
-#pragma unroll 8
-        for (int jj = je - 1; jj >= js; --jj) {
-            const P3 ty = Yb[jj];
-            const float d = sq_dist(x.x, x.y, x.z, ty.x, ty.y, ty.z);
-            found = (d == val) ? jj : found;
+            for (int tb = 0; tb < a.nTB; ++tb) key = min(key, rp[static_cast<int64_t>(tb) * a.N]);
+            val = __uint_as_float(static_cast<uint32_t>(key >> 32));
+            js = static_cast<int>(static_cast<uint32_t>(key));
+            js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
+            const P3 x = reinterpret_cast<const P3 *>(a.X)[t];
+            px = x.x;
+            py = x.y;
+            pz = x.z;
         }
-        dxy[t] = val;
-        ixy[t] = found;
+        const int64_t wbase = t - lane;
+        const int sub = lane & 7;
+#pragma unroll 2
+        for (int r = 0; r < 8; ++r) {
+            const int src = 8 * r + (lane >> 3);
+            const float v = __shfl(val, src, kWave);
+            const int j0 = __shfl(js, src, kWave);
+            const float qx = __shfl(px, src, kWave), qy = __shfl(py, src, kWave);
+            const float qz = __shfl(pz, src, kWave);
+            const int64_t tp = wbase + src;
+            int cand = 0x7fffffff;
+            if (tp < nx) {
+                const int64_t b = tp / a.N;
+                const P3 *Yb = reinterpret_cast<const P3 *>(a.Y + b * a.M * 3);
+                const int je = j0 + min(kBatch, a.M - j0);
+                const int jl = max(je - 1, 0);
+                const int jb = j0 + 4 * sub;
+                P3 ty[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) ty[q] = Yb[min(jb + q, jl)];
+#pragma unroll
+                for (int q = 3; q >= 0; --q) {
+                    const float d = sq_dist(qx, qy, qz, ty[q].x, ty[q].y, ty[q].z);
+                    cand = (jb + q < je && d == v) ? jb + q : cand;
+                }
+            }
+#pragma unroll
+            for (int off = 1; off < 8; off <<= 1) cand = min(cand, __shfl_xor(cand, off, kWave));
+            if (sub == 0 && tp < nx) {
+                dxy[tp] = v;
+                ixy[tp] = cand == 0x7fffffff ? -1 : cand;
+            }
+        }
     } else {
-        const int64_t u = t - nx;
+        const int64_t u = t - nr;
         const int64_t b = u / a.M, jy = u - b * a.M;
         const unsigned long long *cp = a.colpart + b * a.nQG * static_cast<int64_t>(a.M) + jy;
         unsigned long long key = ~0ull;
@@ -390,7 +434,7 @@ hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream
     a.pad = 0;
     a.B = p.B;
     search_kernel<<<static_cast<uint32_t>(forward_tiles(p)), kThreads, 0, stream>>>(a);
-    const int64_t total = p.B * (static_cast<int64_t>(p.N) + p.M);
+    const int64_t total = merge_row_threads(p.B * static_cast<int64_t>(p.N)) + p.B * p.M;
     merge_kernel<<<static_cast<uint32_t>(ceil_div(total, kMergeThreads)), kMergeThreads, 0,
                    stream>>>(a, f.dist_xy, f.idx_xy, f.dist_yx, f.idx_yx);
     return hipGetLastError();
