@@ -193,3 +193,34 @@ def test_full_size_workload_sampled():
     assert np.all(np.abs(dist - dg) <= _tol(dg, R))
     d2, f2 = gpu_p2s(P, V, F)
     assert np.array_equal(d2, dist) and np.array_equal(f2, fidx)
+
+
+def _sweep_cases(seed=4048):
+    """Seeded random shapes: B in 1..4, S log-uniform in [1, 20000], icosphere
+    levels 0..4 (20 to 5120 faces), at most 5e7 point-face pairs each."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < 12:
+        B = int(rng.integers(1, 5))
+        S = int(np.exp(rng.uniform(0, np.log(20000))))
+        level = int(rng.integers(0, 5))
+        if B * S * 20 * 4 ** level <= 5e7:
+            out.append((B, S, level, int(rng.integers(1 << 30))))
+    return out
+
+
+@pytest.mark.parametrize("B,S,level,seed", _sweep_cases())
+def test_random_shape_forward_and_backward(B, S, level, seed):
+    """Forward against the oracle (distance tolerance, face or near-tie) and
+    the backward's exact-sum bound, with a bitwise repeat, on seeded shapes."""
+    print(f"[sweep] p2s B={B} S={S} level={level} seed={seed}", flush=True)
+    P, V, F = synth.p2s_workload(B, S, level, seed)
+    Pg, Vg, Fg = gc.to_gpu(P), gc.to_gpu(V), gc.to_gpu(F)
+    dist, fidx = cd.p2s_forward(Pg, Vg, Fg)
+    nbad = check_forward(P, V, F, gc.to_np(dist), gc.to_np(fidx))
+    assert nbad <= max(2, S * B // 500), nbad
+    g = np.random.default_rng(seed + 1).uniform(0.5, 2.0, (B, S)).astype(np.float32)
+    gP, gV = cd.p2s_backward(Pg, Vg, Fg, fidx, gc.to_gpu(g))
+    gP2, gV2 = cd.p2s_backward(Pg, Vg, Fg, fidx, gc.to_gpu(g))
+    assert torch.equal(gP, gP2) and torch.equal(gV, gV2)
+    _check_backward(P, V, F, gc.to_np(fidx), g, gc.to_np(gP), gc.to_np(gV))
