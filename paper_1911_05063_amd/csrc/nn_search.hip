@@ -23,14 +23,16 @@
 //    lane holding the minimum is found.  The 4 waves combine through a 64-bit
 //    LDS atomicMin on (distance bits << 32 | lane), which orders by distance
 //    then lane because distances are >= +0.
-//  * Target blocks: TB targets (256..512), except the last ones of every
-//    group, which are small (128) and sit at the end of the grid, so that the
-//    final round of workgroups is filled with short tiles.
+//  * Target blocks: TB targets (256..512).  In a launch of one to eight
+//    rounds of resident workgroups, the last targets of every group go to
+//    small blocks (128) at the end of the grid, so that the final round is
+//    filled with short tiles.
 //  * Each tile writes one packed (distance, batch start) key per x-point and
 //    one (distance, lane) key per y-point to the workspace; a merge kernel
 //    takes the minimum key over tiles and recovers the exact lowest index by
-//    recomputing the kBatch candidate targets of a row or the kQ candidate
-//    x-points of a column with the same instructions, so equality is exact.
+//    recomputing the kBatch candidate targets of a row (8 lanes per x-point)
+//    or the kQ candidate x-points of a column with the same instructions, so
+//    equality is exact.
 #include "cd_internal.h"
 
 #include <algorithm>
