@@ -498,24 +498,6 @@ def emd_step_bench(args):
 
 def main():
     args = parse_args()
-    if args.path == "emd":
-        if args.gpus != 1:
-            print("bench.py measures one GPU only", file=sys.stderr)
-            sys.exit(2)
-        emd_step_bench(args)
-        return
-    if args.path == "p2s":
-        if args.gpus != 1:
-            print("bench.py measures one GPU only", file=sys.stderr)
-            sys.exit(2)
-        p2s_step_bench(args)
-        return
-    if args.path == "mesh":
-        if args.gpus != 1:
-            print("bench.py measures one GPU only", file=sys.stderr)
-            sys.exit(2)
-        mesh_step_bench(args)
-        return
     if args.ingest_pmc:
         ingest_pmc(*args.ingest_pmc)
         return
@@ -523,6 +505,15 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the batch items are independent: shard them across GPUs).", file=sys.stderr)
         sys.exit(2)
+    if args.path == "emd":
+        emd_step_bench(args)
+        return
+    if args.path == "p2s":
+        p2s_step_bench(args)
+        return
+    if args.path == "mesh":
+        mesh_step_bench(args)
+        return
     import numpy as np
     import torch
     import synth
