@@ -5,7 +5,8 @@
 // three share one accumulation order and agree bitwise.  One 1024-thread
 // workgroup per item: each thread sums its elements in order (in double: the
 // rows are long, and a float32 running sum over 1e5 terms could drift past
-// 1e-5 relative) with 16 loads in flight, counts come from wave ballots, and
+// 1e-5 relative) with 16 loads in flight (32 for the first group: both
+// arrays at once), counts come from wave ballots, and
 // a single reduction (wave shuffles, then the 16 waves in order) combines
 // everything, so the results are bitwise reproducible.
 #include "cd_internal.h"
@@ -49,9 +50,14 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
     // unrolled by hand because loops holding ballots are not unrolled by the
     // compiler), then single full strides, then one partial stride.  Every
     // lane runs the same trip counts, so the ballots see the full wave.
-    auto pass = [&](const float *p, int64_t n, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1]) {
+    auto take = [&](float v, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1]) {
+        if (do_chamfer) sum += static_cast<double>(v);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v < thr[t]));
+    };
+    auto pass = [&](const float *p, int64_t n, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1],
+                    int64_t s) {
         const int64_t full = n / kBlock;
-        int64_t s = 0;
         for (; s + kGroup <= full; s += kGroup) {
             float v[kGroup];
 #pragma unroll
@@ -76,8 +82,25 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
 #pragma unroll
         for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(in && v < thr[t]));
     };
-    pass(a, N, sx, cp);
-    pass(c, M, sy, cr);
+    // The first group of each array is loaded together (one memory round
+    // instead of two when both arrays have a full group); the sums still take
+    // every array's elements in order.
+    int64_t s0 = 0;
+    if (N / kBlock >= kGroup && M / kBlock >= kGroup) {
+        float va[kGroup], vc[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            va[u] = a[u * kBlock + threadIdx.x];
+            vc[u] = c[u * kBlock + threadIdx.x];
+        }
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) take(va[u], sx, cp);
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) take(vc[u], sy, cr);
+        s0 = kGroup;
+    }
+    pass(a, N, sx, cp, s0);
+    pass(c, M, sy, cr, s0);
     // One reduction for everything: sums over the wave by shuffles (counts are
     // already per wave: every lane holds the wave's ballot totals), then the
     // waves in order.
