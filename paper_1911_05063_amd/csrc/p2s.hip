@@ -102,30 +102,36 @@ __global__ __launch_bounds__(kThreads) void face_record_kernel(int64_t B, int64_
     // e0.g0 = e1.g1 = 1 and e1.g0 = e0.g1 = n.g0 = n.g1 = 0.
     double g0[3] = {0, 0, 0}, g1[3] = {0, 0, 0}, nh[3] = {0, 0, 0};
     const bool flat = !(nn > 0.0) || !std::isfinite(nn);
+    // One reciprocal per denominator (double divisions are long instruction
+    // sequences); the record is rounded to float32 afterwards.
     if (!flat) {
-        g0[0] = (e1[1] * n[2] - e1[2] * n[1]) / nn;
-        g0[1] = (e1[2] * n[0] - e1[0] * n[2]) / nn;
-        g0[2] = (e1[0] * n[1] - e1[1] * n[0]) / nn;
-        g1[0] = (n[1] * e0[2] - n[2] * e0[1]) / nn;
-        g1[1] = (n[2] * e0[0] - n[0] * e0[2]) / nn;
-        g1[2] = (n[0] * e0[1] - n[1] * e0[0]) / nn;
+        const double rn = 1.0 / nn;
+        g0[0] = (e1[1] * n[2] - e1[2] * n[1]) * rn;
+        g0[1] = (e1[2] * n[0] - e1[0] * n[2]) * rn;
+        g0[2] = (e1[0] * n[1] - e1[1] * n[0]) * rn;
+        g1[0] = (n[1] * e0[2] - n[2] * e0[1]) * rn;
+        g1[1] = (n[2] * e0[0] - n[0] * e0[2]) * rn;
+        g1[2] = (n[0] * e0[1] - n[1] * e0[0]) * rn;
         const double inv = 1.0 / sqrt(nn);
         for (int i = 0; i < 3; ++i) nh[i] = n[i] * inv;
     }
     const double l0 = e0[0] * e0[0] + e0[1] * e0[1] + e0[2] * e0[2];
     const double l1 = e1[0] * e1[0] + e1[1] * e1[1] + e1[2] * e1[2];
     const double l2 = e2[0] * e2[0] + e2[1] * e2[1] + e2[2] * e2[2];
+    const double r0 = l0 > 0.0 ? 1.0 / l0 : 0.0;
+    const double r1 = l1 > 0.0 ? 1.0 / l1 : 0.0;
+    const double r2 = l2 > 0.0 ? 1.0 / l2 : 0.0;
     for (int i = 0; i < 3; ++i) {
         r[0 + i] = static_cast<float>(A[i]);
         r[3 + i] = static_cast<float>(g0[i]);
         r[6 + i] = static_cast<float>(g1[i]);
         r[9 + i] = static_cast<float>(nh[i]);
         r[13 + i] = static_cast<float>(e0[i]);
-        r[16 + i] = static_cast<float>(l0 > 0.0 ? e0[i] / l0 : 0.0);
+        r[16 + i] = static_cast<float>(e0[i] * r0);
         r[19 + i] = static_cast<float>(e1[i]);
-        r[22 + i] = static_cast<float>(l1 > 0.0 ? e1[i] / l1 : 0.0);
+        r[22 + i] = static_cast<float>(e1[i] * r1);
         r[25 + i] = static_cast<float>(e2[i]);
-        r[28 + i] = static_cast<float>(l2 > 0.0 ? e2[i] / l2 : 0.0);
+        r[28 + i] = static_cast<float>(e2[i] * r2);
     }
     r[12] = flat ? __builtin_inff() : 0.0f;
     r[31] = 0.0f;
