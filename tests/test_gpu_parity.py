@@ -186,6 +186,28 @@ def test_autograd_chamfer_distance():
                    np.array([1.0, -2.0, 0.5]))
 
 
+@pytest.mark.parametrize("k", [-40, 40])
+def test_power_of_two_scaling_is_exact(k):
+    """Scaling both clouds by 2^k scales every distance by 2^(2k), keeps every
+    index, and scales the gradients by 2^k, all exactly: the float32 arithmetic
+    commutes with power-of-two scaling and the fixed-point shift of the
+    backward moves by k with the terms (local and bounded shifts)."""
+    for B, N, M in ((2, 3000, 2500), (1, 20000, 3000)):
+        X, Y = synth.generate("mesh", B, N, M, 91)
+        s = np.float32(2.0 ** k)
+        Xs, Ys = X * s, Y * s
+        a = gc.gpu_forward(X, Y)
+        b = gc.gpu_forward(Xs, Ys)
+        assert np.array_equal(a[1], b[1]) and np.array_equal(a[3], b[3])
+        assert np.array_equal(a[0].astype(np.float64) * 2.0 ** (2 * k), b[0])
+        assert np.array_equal(a[2].astype(np.float64) * 2.0 ** (2 * k), b[2])
+        go = gc.to_gpu(np.linspace(0.5, 1.5, B).astype(np.float32))
+        idx = (gc.to_gpu(a[1]), gc.to_gpu(a[3]))
+        gX, gY = cd.chamfer_backward(go, gc.to_gpu(X), gc.to_gpu(Y), *idx)
+        hX, hY = cd.chamfer_backward(go, gc.to_gpu(Xs), gc.to_gpu(Ys), *idx)
+        assert torch.equal(gX * 2.0 ** k, hX) and torch.equal(gY * 2.0 ** k, hY)
+
+
 def test_forward_is_bitwise_reproducible():
     X, Y = synth.generate("grid_dup", 4, 4096, 3000, 41)
     a = gc.gpu_forward(X, Y)
