@@ -224,3 +224,21 @@ def test_random_shape_forward_and_backward(B, S, level, seed):
     gP2, gV2 = cd.p2s_backward(Pg, Vg, Fg, fidx, gc.to_gpu(g))
     assert torch.equal(gP, gP2) and torch.equal(gV, gV2)
     _check_backward(P, V, F, gc.to_np(fidx), g, gc.to_np(gP), gc.to_np(gV))
+
+
+@pytest.mark.parametrize("k", [-30, 30])
+def test_power_of_two_scaling_is_exact(k):
+    """Scaling points and vertices by 2^k scales every distance by 2^(2k),
+    keeps every face choice and scales gP and gV by 2^k, exactly (every
+    step, including the float64 face records, commutes with the scaling)."""
+    P, V, F = synth.p2s_workload(2, 3000, 3, 71)
+    s = np.float32(2.0 ** k)
+    d1, f1 = gpu_p2s(P, V, F)
+    d2, f2 = gpu_p2s(P * s, V * s, F)
+    assert np.array_equal(f1, f2)
+    assert np.array_equal(d1.astype(np.float64) * 2.0 ** (2 * k), d2)
+    g = gc.to_gpu(np.random.default_rng(72).uniform(0.5, 2.0, f1.shape).astype(np.float32))
+    fi = gc.to_gpu(f1)
+    gP1, gV1 = cd.p2s_backward(gc.to_gpu(P), gc.to_gpu(V), gc.to_gpu(F), fi, g)
+    gP2, gV2 = cd.p2s_backward(gc.to_gpu(P * s), gc.to_gpu(V * s), gc.to_gpu(F), fi, g)
+    assert torch.equal(gP1 * 2.0 ** k, gP2) and torch.equal(gV1 * 2.0 ** k, gV2)
