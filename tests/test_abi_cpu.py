@@ -266,3 +266,42 @@ def test_launch_size_limits(lib):
     # The EMD gradient merge: one thread per component, 3 B max(N, M) < 2^32.
     assert lib.cd_emd_forward(1, 2 ** 30 + 2 ** 29, 10, FAKE, FAKE, 0.5, 0.01, 1, 0, FAKE, FAKE, FAKE,
                               FAKE, 1 << 40, None) == CD_ERR_INVALID_ARG
+
+
+C_CLIENT = r"""
+#include <stdio.h>
+#include "cd.h"
+int main(void)
+{
+    /* Pure argument checks and sizes: no device work, so no GPU is needed. */
+    size_t ws = cd_workspace_bytes(16, 16384, 16384);
+    cd_status s = cd_forward(1, 0, 5, 0, 0, 0, 0, 0, 0, 0, 0, 0);
+    printf("%s %s %d %s\n", cd_version(), cd_status_string(s), ws > 0, cd_last_error());
+    return s == CD_ERR_INVALID_ARG && ws > 0 ? 0 : 1;
+}
+"""
+
+
+@pytest.mark.parametrize("compiler,std", [("gcc", "-std=c99"), ("g++", "-std=c++17")])
+def test_header_builds_a_c_and_cpp_client(lib, tmp_path, compiler, std):
+    """include/cd.h compiles as C and C++, and a client linked against the
+    library calls it (argument checks only)."""
+    import shutil
+    import subprocess
+    import paper_1911_05063_amd as cd
+    if shutil.which(compiler) is None:
+        pytest.skip(f"{compiler} not available")
+    src = tmp_path / ("client.c" if compiler == "gcc" else "client.cpp")
+    src.write_text(C_CLIENT)
+    exe = tmp_path / "client"
+    libdir = os.path.dirname(cd.LIB_PATH)
+    cmd = [compiler, std, "-Wall", "-Wextra", "-Werror", "-I", os.path.join(ROOT, "include"),
+           str(src), "-o", str(exe), f"-L{libdir}", "-lcd_hip", f"-Wl,-rpath,{libdir}"]
+    if compiler == "gcc":
+        cmd.insert(1, "-x")
+        cmd.insert(2, "c")
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "CD_ERR_INVALID_ARG" in r.stdout and "N < 1" in r.stdout
