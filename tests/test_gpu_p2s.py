@@ -78,9 +78,11 @@ def gpu_p2s(P, V, F):
     return gc.to_np(dist), gc.to_np(fidx)
 
 
-# (8, 4096, 4): 64 blocks of 64 faces, then 64 small blocks of 16 per item.
+# (8, 4096, 4): 64 blocks of 64 faces, then 64 small blocks of 16 per item;
+# (1, 500, 5): 20480 faces in 320 blocks of 64.
 @pytest.mark.parametrize("B,S,level,seed", [(2, 3001, 2, 1), (3, 700, 1, 2), (1, 1, 0, 3),
-                                            (2, 5000, 3, 4), (1, 2049, 4, 5), (8, 4096, 4, 6)])
+                                            (2, 5000, 3, 4), (1, 2049, 4, 5), (8, 4096, 4, 6),
+                                            (1, 500, 5, 7)])
 def test_forward_matches_oracle(B, S, level, seed):
     print(f"[case] p2s B={B} S={S} level={level}", flush=True)
     P, V, F = synth.p2s_workload(B, S, level, seed)
