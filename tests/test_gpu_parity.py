@@ -393,3 +393,38 @@ def test_lattice_closed_form_full_size(B, dims):
     assert np.array_equal(gc.to_np(gX), np.broadcast_to((-k * s).astype(np.float32), X.shape))
     assert np.array_equal(gc.to_np(gY), np.broadcast_to((k * s).astype(np.float32), Y.shape))
     assert np.all(gc.to_np(f) == 1.0)
+
+
+def test_step_can_be_captured_in_a_graph():
+    """The library issues no allocation, memset or synchronization, so a whole
+    step (forward, metrics, backward) can be captured in a HIP graph; every
+    replay, with eager steps and synchronizations between them, equals the
+    eager step bitwise."""
+    X_np, Y_np = synth.generate("sphere", 3, 2500, 1800, 95)
+    X, Y = gc.to_gpu(X_np), gc.to_gpu(Y_np)
+    go = gc.to_gpu(np.array([1.0, 0.5, 2.0], np.float32))
+    ws = torch.empty(cd.workspace_bytes(3, 2500, 1800), dtype=torch.uint8, device="cuda:0")
+
+    def step():
+        dxy, ixy, dyx, iyx = cd.nn_distance(X, Y, ws)
+        ch, f, p, r = cd.metrics(dxy, dyx, (0.01, 0.05))
+        gX, gY = cd.chamfer_backward(go, X, Y, ixy, iyx)
+        return dxy, ixy, dyx, iyx, ch, f, gX, gY
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out = step()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        ref = step()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(out, ref):
+            assert torch.equal(a, b)
