@@ -45,6 +45,9 @@ cd_status check_shape(int64_t B, int64_t N, int64_t M)
     return CD_OK;
 }
 
+// a * b > lim for a, b >= 0, without forming a product that could overflow.
+bool product_exceeds(int64_t a, int64_t b, int64_t lim) { return a > 0 && b > lim / a; }
+
 bool aligned256(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 
 // A float32 squared distance d satisfies d < tau^2 (exact in double for a
@@ -220,7 +223,8 @@ static cd_status check_mesh(int64_t B, int64_t nv, int64_t nf, int64_t S)
     if (nv > kMaxPoints || nf > kMaxPoints || S > kMaxPoints) return invalid("nv, nf or S >= 2^31");
     // Per-sample kernels launch B * S threads and the backward B * ceil(nv / 2048)
     // workgroups (times a bounded number of sample chunks).
-    if (B > 0 && (B * S > (int64_t(1) << 31) || B * ((nv + 2047) / 2048) > (int64_t(1) << 23)))
+    if (product_exceeds(B, S, int64_t(1) << 31) ||
+        product_exceeds(B, (nv + 2047) / 2048, int64_t(1) << 23))
         return invalid("B * S > 2^31 or B * ceil(nv / 2048) > 2^23");
     return CD_OK;
 }
@@ -296,8 +300,8 @@ static cd_status check_p2s(int64_t B, int64_t S, int64_t nv, int64_t nf)
     if (S < 0) return invalid("S < 0");
     if (nv < 1 || nf < 1) return invalid("a mesh needs nv >= 1 and nf >= 1");
     if (nv > kMaxPoints || nf > kMaxPoints || S > kMaxPoints) return invalid("nv, nf or S >= 2^31");
-    if (B > 0 && (B * S > (int64_t(1) << 31) || B * nf > (int64_t(1) << 31) ||
-                  B * ((nv + 2047) / 2048) > (int64_t(1) << 23)))
+    if (product_exceeds(B, S, int64_t(1) << 31) || product_exceeds(B, nf, int64_t(1) << 31) ||
+        product_exceeds(B, (nv + 2047) / 2048, int64_t(1) << 23))
         return invalid("B * S > 2^31, B * nf > 2^31 or B * ceil(nv / 2048) > 2^23");
     return CD_OK;
 }
@@ -367,7 +371,7 @@ cd_status cd_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, const 
     if (!positive_finite(eps_start) || !positive_finite(eps_end))
         return invalid("eps_start and eps_end must be positive and finite");
     if (n_iters < 1) return invalid("n_iters < 1");
-    if (B > 0 && 3 * B * std::max(N, M) > (int64_t(1) << 32) - (int64_t(1) << 20))
+    if (product_exceeds(B, 3 * std::max(N, M), (int64_t(1) << 32) - (int64_t(1) << 20)))
         return invalid("3 B max(N, M) >= 2^32 (one thread per gradient component)");
     if (B == 0) return CD_OK;
     if (!X || !Y || !f || !g || !cost) return invalid("NULL array pointer");
@@ -386,7 +390,7 @@ cd_status cd_emd_backward(int64_t B, int64_t N, int64_t M, const float *X, const
     cd_status s = check_shape(B, N, M);
     if (s != CD_OK) return s;
     if (!positive_finite(eps)) return invalid("eps must be positive and finite");
-    if (B > 0 && 3 * B * std::max(N, M) > (int64_t(1) << 32) - (int64_t(1) << 20))
+    if (product_exceeds(B, 3 * std::max(N, M), (int64_t(1) << 32) - (int64_t(1) << 20)))
         return invalid("3 B max(N, M) >= 2^32 (one thread per gradient component)");
     if (B == 0) return CD_OK;
     if (!X || !Y || !f || !g || !grad_out || !gX || !gY) return invalid("NULL array pointer");

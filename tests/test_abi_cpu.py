@@ -305,3 +305,22 @@ def test_header_builds_a_c_and_cpp_client(lib, tmp_path, compiler, std):
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "CD_ERR_INVALID_ARG" in r.stdout and "N < 1" in r.stdout
+
+
+def test_huge_batch_counts_are_rejected_without_overflow(lib):
+    # B * S (and the like) would wrap around int64 here; the checks must not form it.
+    big = 2 ** 62
+    assert lib.cd_workspace_bytes(big, 2 ** 30, 2 ** 30) == 0
+    assert lib.cd_mesh_workspace_bytes(big, 30, 10, 2 ** 31 - 1) == 0
+    assert lib.cd_mesh_workspace_bytes(big, 2 ** 31 - 1, 10, 0) == 0
+    assert lib.cd_p2s_workspace_bytes(big, 2 ** 31 - 1, 30, 10) == 0
+    assert lib.cd_p2s_workspace_bytes(big, 0, 30, 2 ** 31 - 1) == 0
+    assert lib.cd_emd_workspace_bytes(big, 2 ** 30, 4) == 0
+    assert lib.cd_emd_forward(big, 4, 2 ** 31 - 1, FAKE, FAKE, 0.5, 0.01, 1, 0, FAKE, FAKE, FAKE,
+                              FAKE, 1 << 40, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_emd_backward(big, 4, 2 ** 31 - 1, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, FAKE, FAKE,
+                               FAKE, 1 << 40, None) == CD_ERR_INVALID_ARG
+    assert lib.cd_p2s_forward(big, 2 ** 31 - 1, 3, 1, *([FAKE] * 5), FAKE, 1 << 40,
+                              None) == CD_ERR_INVALID_ARG
+    assert lib.cd_mesh_sample_points(big, 3, 4, FAKE, FAKE, 2 ** 31 - 1, FAKE, FAKE, FAKE, FAKE,
+                                     None) == CD_ERR_INVALID_ARG
