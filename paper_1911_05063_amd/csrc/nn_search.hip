@@ -268,7 +268,10 @@ __host__ __device__ __forceinline__ int64_t merge_row_threads(int64_t nx)
 // column.  A wave of rows takes the minimum key of its 64 x-points (one per
 // lane), then rescans their candidate batches 8 x-points at a time: 8 lanes
 // per x-point, each lane 4 consecutive targets (48 contiguous bytes), and the
-// lowest matching index over the 8 lanes.
+// lowest matching index over the 8 lanes.  The rescan loads are clamped into
+// the cloud instead of guarded, so that two rounds' loads are in flight
+// together.  The partial keys are read once: non-temporal loads keep them
+// from evicting the coordinates that the rescans read.
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
                                                               int32_t *ixy, float *dyx,
@@ -283,13 +286,15 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         const int lane = threadIdx.x % kWave;
         const bool mine = t < nx;
         float val = 0.0f, px = 0.0f, py = 0.0f, pz = 0.0f;
-        int js = a.M;
+        int js = a.M, bi = 0;  // candidate batch start (M: none) and item
         if (mine) {
             const int64_t b = t / a.N, i = t - b * a.N;
+            bi = static_cast<int>(b);
             const unsigned long long *rp = a.rowpart + b * a.nTB * static_cast<int64_t>(a.N) + i;
             unsigned long long key = ~0ull;
 #pragma unroll 8
-            for (int tb = 0; tb < a.nTB; ++tb) key = min(key, rp[static_cast<int64_t>(tb) * a.N]);
+            for (int tb = 0; tb < a.nTB; ++tb)
+                key = min(key, __builtin_nontemporal_load(rp + static_cast<int64_t>(tb) * a.N));
             val = __uint_as_float(static_cast<uint32_t>(key >> 32));
             js = static_cast<int>(static_cast<uint32_t>(key));
             js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
@@ -300,35 +305,51 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         }
         const int64_t wbase = t - lane;
         const int sub = lane & 7;
-#pragma unroll 2
-        for (int r = 0; r < 8; ++r) {
-            const int src = 8 * r + (lane >> 3);
-            const float v = __shfl(val, src, kWave);
-            const int j0 = __shfl(js, src, kWave);
-            const float qx = __shfl(px, src, kWave), qy = __shfl(py, src, kWave);
-            const float qz = __shfl(pz, src, kWave);
-            const int64_t tp = wbase + src;
-            int cand = 0x7fffffff;
-            if (tp < nx) {
-                const int64_t b = tp / a.N;
-                const P3 *Yb = reinterpret_cast<const P3 *>(a.Y + b * a.M * 3);
-                const int je = j0 + min(kBatch, a.M - j0);
-                const int jl = max(je - 1, 0);
-                const int jb = j0 + 4 * sub;
-                P3 ty[4];
+        constexpr int kR = 2;  // rescan rounds whose loads are issued together
+        for (int r0 = 0; r0 < 8; r0 += kR) {
+            float v[kR], qx[kR], qy[kR], qz[kR];
+            int je[kR], jb[kR];
+            P3 ty[kR][4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) ty[q] = Yb[min(jb + q, jl)];
+            for (int r = 0; r < kR; ++r) {
+                const int src = 8 * (r0 + r) + (lane >> 3);
+                v[r] = __shfl(val, src, kWave);
+                const int j0 = __shfl(js, src, kWave);
+                const int bs = __shfl(bi, src, kWave);
+                qx[r] = __shfl(px, src, kWave);
+                qy[r] = __shfl(py, src, kWave);
+                qz[r] = __shfl(pz, src, kWave);
+                const P3 *Yb =
+                    reinterpret_cast<const P3 *>(a.Y + static_cast<int64_t>(bs) * a.M * 3);
+                // A lane past B*N has j0 = M: every load is target M-1 of item
+                // 0 and no candidate qualifies.
+                je[r] = j0 + min(kBatch, a.M - j0);
+                const int jl = max(je[r] - 1, 0);
+                jb[r] = j0 + 4 * sub;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) ty[r][q] = Yb[min(jb[r] + q, jl)];
+            }
+            int cand[kR];
+#pragma unroll
+            for (int r = 0; r < kR; ++r) {
+                cand[r] = 0x7fffffff;
 #pragma unroll
                 for (int q = 3; q >= 0; --q) {
-                    const float d = sq_dist(qx, qy, qz, ty[q].x, ty[q].y, ty[q].z);
-                    cand = (jb + q < je && d == v) ? jb + q : cand;
+                    const float d =
+                        sq_dist(qx[r], qy[r], qz[r], ty[r][q].x, ty[r][q].y, ty[r][q].z);
+                    cand[r] = (jb[r] + q < je[r] && d == v[r]) ? jb[r] + q : cand[r];
                 }
+#pragma unroll
+                for (int off = 1; off < 8; off <<= 1)
+                    cand[r] = min(cand[r], __shfl_xor(cand[r], off, kWave));
             }
 #pragma unroll
-            for (int off = 1; off < 8; off <<= 1) cand = min(cand, __shfl_xor(cand, off, kWave));
-            if (sub == 0 && tp < nx) {
-                dxy[tp] = v;
-                ixy[tp] = cand == 0x7fffffff ? -1 : cand;
+            for (int r = 0; r < kR; ++r) {
+                const int64_t tp = wbase + 8 * (r0 + r) + (lane >> 3);
+                if (sub == 0 && tp < nx) {
+                    dxy[tp] = v[r];
+                    ixy[tp] = cand[r] == 0x7fffffff ? -1 : cand[r];
+                }
             }
         }
     } else {
@@ -337,7 +358,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         const unsigned long long *cp = a.colpart + b * a.nQG * static_cast<int64_t>(a.M) + jy;
         unsigned long long key = ~0ull;
 #pragma unroll 8
-        for (int q = 0; q < a.nQG; ++q) key = min(key, cp[static_cast<int64_t>(q) * a.M]);
+        for (int q = 0; q < a.nQG; ++q)
+            key = min(key, __builtin_nontemporal_load(cp + static_cast<int64_t>(q) * a.M));
         const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
         // Candidates: the kQ x-points of the winning lane, as a fixed-length,
         // fully unrolled scan (indices clamped to the last one) so that all
