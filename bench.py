@@ -132,25 +132,86 @@ def traffic_record(kernel_sources):
     return rec
 
 
+def _loaded_hip_runtime():
+    """Path of the HIP runtime this process has loaded (torch's), so that the
+    events below live in the same runtime as the streams they are recorded on."""
+    with open("/proc/self/maps") as f:
+        for line in f:
+            path = line.split()[-1]
+            if os.path.basename(path).startswith("libamdhip64.so"):
+                return path
+    raise RuntimeError("the HIP runtime is not loaded (import torch and use the GPU first)")
+
+
+class HipEvent:
+    """A HIP timing event recorded without the system-scope release fence
+    (hipEventDisableSystemFence).  Recording a default event (what
+    torch.cuda.Event creates) writes back and invalidates the L2 cache: about
+    2.4 us of GPU time between two calls, against about 1.2 us for this one;
+    the intervals measured are the same.  Same methods as torch.cuda.Event."""
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def _runtime(cls):
+        if cls._hip is None:
+            hip = ctypes.CDLL(_loaded_hip_runtime())
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        self._h = ctypes.c_void_p()
+        rc = self._runtime().hipEventCreateWithFlags(ctypes.byref(self._h), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self, stream):
+        rc = self._hip.hipEventRecord(self._h, ctypes.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        rc = self._hip.hipEventElapsedTime(ctypes.byref(ms), self._h, end._h)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        try:
+            if self._h and HipEvent._hip is not None:
+                HipEvent._hip.hipEventDestroy(self._h)
+                self._h = ctypes.c_void_p()
+        except Exception:  # interpreter shutdown: nothing left to release
+            pass
+
+
 def timed_steps(one, n_marks, steps, warmup, stream):
     """Warm-up, then exactly `steps` timed steps between two synchronizations.
 
     one(ev) runs a step and records the n_marks events of `ev` (None: no
-    events).  Every event is created before the warm-up, so the timed steps
-    follow the warm-up's synchronization without an idle gap: after a few
-    milliseconds idle the GPU clock drops and needs tens of calls to ramp
-    back up.  Returns (per-step events, total ms, wall seconds)."""
+    events).  Each recorded event costs about a microsecond of GPU time, so
+    the timed steps record only the events their figures need.  Every event
+    is created before the warm-up, so the timed steps follow the warm-up's
+    synchronization without an idle gap: after a few milliseconds idle the GPU
+    clock drops and needs tens of calls to ramp back up.  Returns (per-step
+    events, total ms, wall seconds)."""
     import torch
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_marks)] for _ in range(steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [[HipEvent() for _ in range(n_marks)] for _ in range(steps)]
+    start, stop = HipEvent(), HipEvent()
     for _ in range(warmup):
         one(None)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
     for k in range(steps):
-        one(evs[k])
+        one(evs[k] if n_marks else None)
     stop.record(stream)
     torch.cuda.synchronize()
     return evs, start.elapsed_time(stop), time.perf_counter() - t0
@@ -288,8 +349,10 @@ def mesh_step_bench(args):
         if ev is not None:
             ev[3].record(stream)
 
-    evs, total_ms, _ = timed_steps(one, 4, args.steps, args.warmup, stream)
+    _, total_ms, _ = timed_steps(one, 0, args.steps, args.warmup, stream)
     ms = total_ms / args.steps
+    nb = min(args.steps, 50)
+    evs, _, _ = timed_steps(one, 4, nb, args.warmup, stream)  # per-call breakdown, after the timed steps
     samp = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
     cham = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
     sbwd = statistics.mean(e[2].elapsed_time(e[3]) for e in evs)
@@ -303,7 +366,7 @@ def mesh_step_bench(args):
            "config": {"workload": "mesh_sampling_b16_t200_s16384", "B": B, "triangles": T,
                       "samples": S, "M": M, "taus": [0.005, 0.01, 0.02]},
            "ms_per_call": {"sample_faces+points": samp, "chamfer_fwd_metrics_bwd": cham,
-                           "sample_backward": sbwd},
+                           "sample_backward": sbwd, "breakdown_steps": nb},
            "pct_fp32_valu_peak": 100.0 * FLOPS_PER_PAIR * pairs / (ms * 1e-3) / (PEAK_FP32_TFLOPS * 1e12)}
     print(json.dumps(out), flush=True)
 
@@ -375,15 +438,13 @@ def p2s_step_bench(args):
                          ptr(loss), st), "reduce")
         ok(lib.cd_p2s_backward(B, S, nv, nf, ptr(P), ptr(V), ptr(F), ptr(fidx), ptr(gdist),
                                ptr(gP), ptr(gV), ptr(ws), ws.numel(), st), "backward")
-        if ev is not None:
-            ev[2].record(stream)
 
     print(f"[bench] {w.name}: B={B} S={S} nv={nv} nf={nf} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    evs, total_ms, _ = timed_steps(one, 3, args.steps, args.warmup, stream)
+    evs, total_ms, _ = timed_steps(one, 2, args.steps, args.warmup, stream)
     ms = total_ms / args.steps
     fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
-    rest = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
+    rest = ms - fwd
     pairs = float(B) * S * nf
     achieved = P2S_FLOPS_PER_PAIR * pairs / (fwd * 1e-3) / 1e12
     out = {"metric": "point-to-surface loss step point-triangle pair-evals/sec "
@@ -464,15 +525,13 @@ def emd_step_bench(args):
             ev[1].record(stream)
         ok(lib.cd_emd_backward(B, N, M, ptr(X), ptr(Y), ptr(f), ptr(g), EMD_EPS[1], ptr(go),
                                ptr(gX), ptr(gY), ptr(ws), ws.numel(), st), "backward")
-        if ev is not None:
-            ev[2].record(stream)
 
     print(f"[bench] emd on {w.describe()} iters={EMD_ITERS} eps={EMD_EPS} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    evs, total_ms, _ = timed_steps(one, 3, args.steps, args.warmup, stream)
+    evs, total_ms, _ = timed_steps(one, 2, args.steps, args.warmup, stream)
     ms = total_ms / args.steps
     fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
-    bwd = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
+    bwd = ms - fwd
     pairs = float(B) * N * M * (2 * EMD_ITERS + 3)
     lse_pairs = float(B) * N * M * 2 * EMD_ITERS
     # The forward is dominated by the 2 * iters log-sum-exp passes; price them
@@ -535,16 +594,21 @@ def main():
         if ev is not None:
             ev[1].record(step.stream)
         step.reduce_fscore()
-        if ev is not None:
+        if ev is not None and len(ev) > 2:
             ev[2].record(step.stream)
         step.backward()
-        if ev is not None:
+        if ev is not None and len(ev) > 2:
             ev[3].record(step.stream)
 
-    evs, total_ms, wall = timed_steps(one_step, 4, args.steps, args.warmup, step.stream)
+    # The timed steps record the two events around cd_forward (the roofline's
+    # launch duration); a short pass after them (its own warm-up: the GPU
+    # clock drops while its events are created) times metrics and backward.
+    evs, total_ms, wall = timed_steps(one_step, 2, args.steps, args.warmup, step.stream)
     fwd = [e[0].elapsed_time(e[1]) for e in evs]
-    red = [e[1].elapsed_time(e[2]) for e in evs]
-    bwd = [e[2].elapsed_time(e[3]) for e in evs]
+    nb = min(args.steps, 50)
+    bd, _, _ = timed_steps(one_step, 4, nb, args.warmup, step.stream)
+    red = [e[1].elapsed_time(e[2]) for e in bd]
+    bwd = [e[2].elapsed_time(e[3]) for e in bd]
 
     if args.calib_copy > 0:
         n = args.calib_copy * (1 << 20) // 4
@@ -579,7 +643,7 @@ def main():
                    "taus": list(w.taus), "seed": w.seed},
         "ms_per_call": {"forward": statistics.mean(fwd), "forward_median": statistics.median(fwd),
                         "reduce_fscore": statistics.mean(red), "backward": statistics.mean(bwd),
-                        "fwd_bwd": ms_per_step},
+                        "fwd_bwd": ms_per_step, "breakdown_steps": nb},
         "pct_fp32_valu_peak": 100.0 * FLOPS_PER_PAIR * value / (PEAK_FP32_TFLOPS * 1e12),
         "wall_s": wall,
         "roofline": {"bound": "alu", "kernel": "cd_forward (search_kernel + merge_kernel)",
