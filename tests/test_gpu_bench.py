@@ -1,0 +1,37 @@
+"""bench.py on the GPU: each path runs a few steps and prints one JSON line with
+the fields its consumers read (a child process, as the benchmark is run)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("args", [[], ["--path", "mesh"], ["--path", "p2s"], ["--path", "emd"]],
+                         ids=["chamfer", "mesh", "p2s", "emd"])
+def test_bench_prints_one_json_line(args):
+    cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "3", "--warmup", "2",
+           "--no-cpu-baseline"] + args
+    print("[bench test]", " ".join(cmd[1:]), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=240, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
+    assert len(lines) == 1, r.stdout
+    out = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config"):
+        assert key in out, key
+    assert out["n_gpus"] == 1 and out["steps"] == 3 and out["warmup"] == 2
+    assert out["value"] > 0 and out["ms_per_step"] > 0
+    assert "workload" in out["config"]
+    calls = out["ms_per_call"]
+    assert all(v > 0 for k, v in calls.items() if isinstance(v, float)), calls
+    if "roofline" in out:
+        rl = out["roofline"]
+        assert rl["bound"] == "alu" and rl["unit"] == "TFLOP/s" and rl["peak"] == 157.3
+        assert 0 < rl["frac"] < 1.0 and abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-9
