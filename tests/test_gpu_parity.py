@@ -273,19 +273,28 @@ def test_extreme_shapes(B, N, M):
     gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), f"B{B}-N{N}-M{M}")
 
 
-def test_target_cloud_past_2pow30_points():
-    # M = 2^30 + 3 y-points (3*M floats > 2^31): 64-bit addressing at the
-    # largest size that fits comfortably.  Built on the GPU; closed form: the
-    # bulk of Y sits at (100,100,100), three planted points lie near x-points.
-    M = (1 << 30) + 3
+BIG_M = (1 << 30) + 3
+BIG_FAR, BIG_MID = BIG_M - 1, 800_000_123
+
+
+def _big_target_cloud():
+    """M = 2^30 + 3 y-points (3*M floats > 2^31), built on the GPU: the bulk of
+    Y sits at (100,100,100), three planted points lie near x-points."""
     dev = "cuda:0"
     X = torch.tensor([[[0, 0, 0], [4, 0, 0], [0, 4, 0], [0, 0, 4], [-4, 0, 0]]],
                      dtype=torch.float32, device=dev)
-    Y = torch.full((1, M, 3), 100.0, dtype=torch.float32, device=dev)
-    far, mid = M - 1, 800_000_123
-    Y[0, far] = torch.tensor([0.25, 0.0, 0.0], device=dev)
-    Y[0, mid] = torch.tensor([4.0, 0.5, 0.0], device=dev)
+    Y = torch.full((1, BIG_M, 3), 100.0, dtype=torch.float32, device=dev)
+    Y[0, BIG_FAR] = torch.tensor([0.25, 0.0, 0.0], device=dev)
+    Y[0, BIG_MID] = torch.tensor([4.0, 0.5, 0.0], device=dev)
     Y[0, 2] = torch.tensor([0.0, 4.0, 0.125], device=dev)
+    return X, Y
+
+
+def test_target_cloud_past_2pow30_points():
+    # 64-bit addressing at the largest size that fits comfortably; closed form.
+    M, far, mid = BIG_M, BIG_FAR, BIG_MID
+    dev = "cuda:0"
+    X, Y = _big_target_cloud()
     dxy, ixy, dyx, iyx = cd.nn_distance(X, Y)
     torch.cuda.synchronize()
     assert dxy.cpu().tolist() == [[0.0625, 0.25, 0.015625, 16.0625, 18.0625]]
@@ -298,6 +307,69 @@ def test_target_cloud_past_2pow30_points():
     want_i[special] = torch.tensor([2, 1, 0], dtype=torch.int32, device=dev)
     assert torch.equal(dyx[0], want_d) and torch.equal(iyx[0], want_i)
     del X, Y, dxy, ixy, dyx, iyx, want_d, want_i
+    torch.cuda.empty_cache()
+
+
+def test_backward_past_2pow30_points():
+    # The backward on the same cloud: 2^30 senders scatter into x_1 (64-bit
+    # sender offsets, exact fixed-point sums of 2^30 equal terms) and every
+    # y-point gets its own term.  Closed form in float64 from the forward's
+    # neighbours (grad_out = 1, w1 = w2 = 1): g_xy = 2/N, g_yx = 2/M.
+    M, far, mid, N = BIG_M, BIG_FAR, BIG_MID, 5
+    X, Y = _big_target_cloud()
+    dxy, ixy, dyx, iyx = cd.nn_distance(X, Y)
+    del dxy, dyx
+    gX, gY = cd.chamfer_backward(torch.ones(1, device="cuda:0"), X, Y, ixy, iyx)
+    torch.cuda.synchronize()
+    a, c = 2.0 / N, 2.0 / M
+    x = np.array([[0, 0, 0], [4, 0, 0], [0, 4, 0], [0, 0, 4], [-4, 0, 0]], dtype=np.float64)
+    y_far, y_mid, y_2 = np.array([0.25, 0, 0]), np.array([4.0, 0.5, 0]), np.array([0, 4.0, 0.125])
+    bulk = np.array([100.0, 100.0, 100.0])
+    want_x = np.stack([
+        a * (x[0] - y_far) - c * (y_far - x[0]),
+        a * (x[1] - y_mid) - c * ((M - 3) * (bulk - x[1]) + (y_mid - x[1])),
+        a * (x[2] - y_2) - c * (y_2 - x[2]),
+        a * (x[3] - y_far),
+        a * (x[4] - y_far)])
+    got_x = gX[0].double().cpu().numpy()
+    np.testing.assert_allclose(got_x, want_x, rtol=4e-7, atol=1e-12)
+    want_special = {
+        2: (c + a) * (y_2 - x[2]),
+        mid: (c + a) * (y_mid - x[1]),
+        far: c * (y_far - x[0]) - a * ((x[0] - y_far) + (x[3] - y_far) + (x[4] - y_far))}
+    idx = torch.tensor(sorted(want_special), device="cuda:0")
+    got_special = gY[0, idx].double().cpu().numpy()
+    np.testing.assert_allclose(got_special, np.stack([want_special[k] for k in sorted(want_special)]),
+                               rtol=4e-7, atol=1e-12)
+    # Every bulk y-point: its own term only, c * (y - x_1) = c * (96, 100, 100).
+    gY[0, idx] = torch.tensor(c * (bulk - x[1]), dtype=torch.float32, device="cuda:0")
+    want_bulk = torch.tensor(c * (bulk - x[1]), dtype=torch.float32, device="cuda:0")
+    for k in range(3):
+        dev_k = (gY[0, :, k] - want_bulk[k]).abs().max().item()
+        assert dev_k <= 2.0 ** -22 * float(want_bulk[k]), (k, dev_k)  # two roundings
+    del X, Y, ixy, iyx, gX, gY
+    torch.cuda.empty_cache()
+
+
+def test_query_cloud_past_2pow30_points_mirrors_the_target_case():
+    # N = 2^30 + 3 x-points: the row side of the search, the merge and the
+    # backward at 64-bit offsets.  Swapping the clouds swaps the outputs
+    # bitwise (the same arithmetic on the same pairs; w1 = w2 = 1).
+    Xs, Yb = _big_target_cloud()
+    one = torch.ones(1, device="cuda:0")
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xs, Yb)
+    gXs, gYb = cd.chamfer_backward(one, Xs, Yb, ixy, iyx)
+    del dxy, dyx, ixy, iyx
+    torch.cuda.empty_cache()
+    ref = (gXs, gYb)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Yb, Xs)
+    gYb2, gXs2 = cd.chamfer_backward(one, Yb, Xs, ixy, iyx)
+    torch.cuda.synchronize()
+    assert dxy.shape == (1, BIG_M) and dyx.shape == (1, 5)
+    assert ixy[0, 2].item() == 2 and ixy[0, BIG_MID].item() == 1 and ixy[0, BIG_FAR].item() == 0
+    assert iyx[0].cpu().tolist() == [BIG_FAR, BIG_MID, 2, BIG_FAR, BIG_FAR]
+    assert torch.equal(gXs2, ref[0]) and torch.equal(gYb2, ref[1])
+    del Xs, Yb, dxy, ixy, dyx, iyx, gXs, gYb, gYb2, gXs2, ref
     torch.cuda.empty_cache()
 
 
