@@ -23,10 +23,12 @@
 //    lane holding the minimum is found.  The 4 waves combine through a 64-bit
 //    LDS atomicMin on (distance bits << 32 | lane), which orders by distance
 //    then lane because distances are >= +0.
-//  * Target blocks: TB targets (256..512).  In a launch of one to eight
-//    rounds of resident workgroups, the last targets of every group go to
-//    small blocks (128) at the end of the grid, so that the final round is
-//    filled with short tiles.
+//  * Target blocks: TB targets (256..512), aiming at about four rounds of
+//    resident workgroups.  In a launch of one to eight rounds, the last
+//    targets of every group go to small blocks (128) at the end of the grid,
+//    so that the final round is filled with short tiles.  A problem too small
+//    for one round gets blocks of 32..512 targets, about half a round of
+//    tiles.
 //  * Each tile writes one packed (distance, batch start) key per x-point and
 //    one (distance, lane) key per y-point to the workspace; a merge kernel
 //    takes the minimum key over tiles and recovers the exact lowest index by
@@ -51,6 +53,7 @@ constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (4 rounds of 4 
 constexpr int64_t kSlots = 256 * 4;     // workgroups resident at once: 256 CUs x 4
 constexpr int kSmallTB = 128;           // targets per block of the final, small tiles
 constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of 1 to 8 rounds
+constexpr int64_t kSmallLaunchTiles = 512;  // tiles to aim for below one round
 constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
@@ -413,10 +416,23 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
     const int64_t want_blocks = ceil_div(kTargetTiles, groups);
     int64_t TB = ceil_div(ceil_div(M, want_blocks), kBatch) * kBatch;
     TB = std::min<int64_t>(std::max<int64_t>(TB, kMinTB), kMaxTB);
+    int64_t blocks = ceil_div(M, TB);
+    if (groups * blocks < kSlots) {
+        // Not one round even with kMinTB: smaller blocks (down to one batch)
+        // until there are about half a round of tiles (two waves per SIMD).
+        // More and smaller tiles measured slower: per-tile set-up and partial
+        // keys grow faster than the parallelism helps.
+        const int64_t ts = std::max<int64_t>(
+            kBatch,
+            ceil_div(ceil_div(M, ceil_div(kSmallLaunchTiles, groups)), kBatch) * kBatch);
+        if (ts < TB) {
+            TB = ts;
+            blocks = ceil_div(M, TB);
+        }
+    }
     p.TB = static_cast<int32_t>(TB);
     p.TS = kSmallTB;
-    const int64_t blocks = ceil_div(M, TB);
-    if (groups * blocks >= kSlots && groups * blocks <= kSmallRounds * kSlots) {
+    if (TB > kSmallTB && groups * blocks >= kSlots && groups * blocks <= kSmallRounds * kSlots) {
         // A launch of one to a few rounds: the last targets of every group go
         // to small blocks, about a quarter round of resident workgroups' worth
         // of work.
