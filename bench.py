@@ -55,6 +55,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--cpu-items", type=int, default=0,
                     help="batch items in the CPU-oracle sample (0 = all items)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="repeat the CPU-oracle sample until this much time has passed")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="read two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; each with "
                          "--calib-copy 256), write profiles/traffic_mesh_b16_n16384.json, exit")
@@ -280,22 +282,37 @@ class Step:
                                       self.bws_bytes, self.s), "cd_backward")
 
 
-def time_cpu_oracle(X, Y, taus, items):
+def repeat_for(run_once, seconds):
+    """Run run_once() until `seconds` have passed (at least once); returns
+    (repetitions, elapsed seconds)."""
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        run_once()
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= seconds:
+            return reps, dt
+
+
+def time_cpu_oracle(X, Y, taus, items, seconds):
     """The CPU oracle (as it stands) on `items` batch items of the workload:
-    nearest neighbours both ways, Chamfer, F-score at each tau, backward."""
+    nearest neighbours both ways, Chamfer, F-score at each tau, backward;
+    repeated for about `seconds`."""
     import numpy as np
     import oracle
     Xs, Ys = X[:items], Y[:items]
     oracle.nn_one_way(Xs[:, :8], Ys[:, :8])  # load + spin up the thread pool
-    t0 = time.perf_counter()
-    r = oracle.forward_all(Xs, Ys, taus)
-    oracle.backward(np.ones(items), Xs, Ys, r["idx_xy"], r["idx_yx"])
-    dt = time.perf_counter() - t0
-    pairs = 2.0 * items * X.shape[1] * Y.shape[1]
+
+    def once():
+        r = oracle.forward_all(Xs, Ys, taus)
+        oracle.backward(np.ones(items), Xs, Ys, r["idx_xy"], r["idx_yx"])
+
+    reps, dt = repeat_for(once, seconds)
+    pairs = 2.0 * items * X.shape[1] * Y.shape[1] * reps
     return {"value": pairs / dt, "unit": "pair-evals/s", "cores": oracle.threads(),
             "kind": "oracle", "seconds": round(dt, 3),
-            "sample": (f"{items} of {X.shape[0]} batch items (N={X.shape[1]}, M={Y.shape[1]}): "
-                       f"float32 nearest neighbours both ways, Chamfer, F-score at "
+            "sample": (f"{items} of {X.shape[0]} batch items (N={X.shape[1]}, M={Y.shape[1]}), "
+                       f"{reps} times: float32 nearest neighbours both ways, Chamfer, F-score at "
                        f"{len(taus)} thresholds and backward, OpenMP over queries")}
 
 
@@ -379,21 +396,24 @@ def mesh_step_bench(args):
 P2S_FLOPS_PER_PAIR = 85
 
 
-def time_cpu_p2s(P, V, F, items, points):
+def time_cpu_p2s(P, V, F, items, points, seconds):
     """The oracle's point-to-surface forward + backward on a bounded sample:
-    the first `points` points of each of the first `items` items."""
+    the first `points` points of each of the first `items` items, repeated
+    for about `seconds`."""
     import numpy as np
     import oracle
     Ps, Vs, Fs = P[:items, :points], V[:items], F[:items]
-    t0 = time.perf_counter()
-    dist, fidx, _ = oracle.p2s_forward(Ps, Vs, Fs)
-    oracle.p2s_backward(Ps, Vs, Fs, fidx, np.full(fidx.shape, 1.0 / points))
-    dt = time.perf_counter() - t0
-    pairs = float(items) * points * F.shape[1]
+
+    def once():
+        dist, fidx, _ = oracle.p2s_forward(Ps, Vs, Fs)
+        oracle.p2s_backward(Ps, Vs, Fs, fidx, np.full(fidx.shape, 1.0 / points))
+
+    reps, dt = repeat_for(once, seconds)
+    pairs = float(items) * points * F.shape[1] * reps
     return {"value": pairs / dt, "unit": "point-triangle pair-evals/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"{items} items x {points} points x {F.shape[1]} faces, forward + backward, "
-                      f"OpenMP over points"}
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"{items} items x {points} points x {F.shape[1]} faces, {reps} times, "
+                      f"forward + backward, OpenMP over points"}
 
 
 def p2s_step_bench(args):
@@ -461,7 +481,7 @@ def p2s_step_bench(args):
                         "work_per_launch": f"{P2S_FLOPS_PER_PAIR} flop x {pairs:.4g} "
                                            f"point-triangle pairs"}}
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = time_cpu_p2s(P_np, V_np, F_np, B, S // 2)
+        out["cpu_baseline"] = time_cpu_p2s(P_np, V_np, F_np, B, S, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
@@ -472,16 +492,23 @@ EMD_FLOPS_PER_PAIR = 15
 EMD_ITERS, EMD_EPS = 50, (0.5, 0.01)
 
 
-def time_cpu_emd(X, Y, items):
-    """The oracle's scheduled Sinkhorn + backward on the first `items` items."""
+def time_cpu_emd(X, Y, seconds):
+    """The oracle's scheduled Sinkhorn + backward, one batch item at a time
+    (items 0, 1, ... in turn) for about `seconds`."""
     import numpy as np
     from oracle import emd_oracle
-    t0 = time.perf_counter()
-    cost, F, G = emd_oracle.sinkhorn(X[:items], Y[:items], EMD_EPS[0], EMD_EPS[1], EMD_ITERS)
-    emd_oracle.backward(X[:items], Y[:items], F, G, EMD_EPS[1], np.ones(items))
-    dt = time.perf_counter() - t0
+    done = [0]
+
+    def once():
+        b = done[0] % X.shape[0]
+        cost, F, G = emd_oracle.sinkhorn(X[b:b + 1], Y[b:b + 1], EMD_EPS[0], EMD_EPS[1], EMD_ITERS)
+        emd_oracle.backward(X[b:b + 1], Y[b:b + 1], F, G, EMD_EPS[1], np.ones(1))
+        done[0] += 1
+
+    items, dt = repeat_for(once, seconds)
     pairs = float(items) * X.shape[1] * Y.shape[1] * (2 * EMD_ITERS + 3)
     return {"value": pairs / dt, "unit": "Sinkhorn pair-evals/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3),
             "sample": f"{items} items x {X.shape[1]} x {Y.shape[1]} points, {EMD_ITERS} iterations "
                       f"+ cost + backward (NumPy float64, dense cost matrix)"}
 
@@ -551,7 +578,7 @@ def emd_step_bench(args):
                         "work_per_launch": f"{EMD_FLOPS_PER_PAIR} flop x {lse_pairs:.4g} "
                                            f"log-sum-exp pair terms"}}
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = time_cpu_emd(X_np, Y_np, 1)
+        out["cpu_baseline"] = time_cpu_emd(X_np, Y_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
@@ -658,7 +685,8 @@ def main():
     if not args.no_cpu_baseline:
         items = args.cpu_items if args.cpu_items > 0 else B
         print(f"[bench] CPU oracle baseline on {items} item(s)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = time_cpu_oracle(X_np, Y_np, w.taus, min(items, B))
+        out["cpu_baseline"] = time_cpu_oracle(X_np, Y_np, w.taus, min(items, B),
+                                              args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
