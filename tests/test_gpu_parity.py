@@ -500,3 +500,34 @@ def test_step_can_be_captured_in_a_graph():
         torch.cuda.synchronize()
         for a, b in zip(out, ref):
             assert torch.equal(a, b)
+
+
+def test_concurrent_streams_match_sequential_runs():
+    # The library keeps no state between calls: two problems interleaved on two
+    # streams (each call with its own workspace and outputs) give the same bits
+    # as each problem run alone.
+    shapes = [("mesh", 3, 5000, 7000, 81), ("gmm", 2, 9000, 3000, 82)]
+    clouds = [tuple(gc.to_gpu(a) for a in synth.generate(k, B, N, M, seed))
+              for k, B, N, M, seed in shapes]
+    one = torch.ones(3, device="cuda:0")
+
+    def step(X, Y):
+        d = cd.nn_distance(X, Y)
+        ch = cd.chamfer_reduce(d[0], d[2])
+        gX, gY = cd.chamfer_backward(one[:X.shape[0]], X, Y, d[1], d[3])
+        return d + (ch, gX, gY)
+
+    ref = [step(X, Y) for X, Y in clouds]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    outs = [[], []]
+    for _ in range(4):
+        for k, (X, Y) in enumerate(clouds):
+            with torch.cuda.stream(streams[k]):
+                outs[k].append(step(X, Y))
+    torch.cuda.synchronize()
+    for k in range(2):
+        for rep in outs[k]:
+            for a, b in zip(rep, ref[k]):
+                assert torch.equal(a, b), shapes[k]
