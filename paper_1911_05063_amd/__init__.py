@@ -133,6 +133,50 @@ def _cloud(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
+def _expect(t: torch.Tensor, name: str, dtype: torch.dtype, shape, device: torch.device
+            ) -> torch.Tensor:
+    """A contiguous tensor of exactly `shape` on `device`: the kernels index
+    every array by the sizes they are given, so a smaller one would be read or
+    written out of bounds."""
+    t = _device_tensor(t, name, dtype)
+    shape = tuple(int(n) for n in shape)
+    if tuple(t.shape) != shape:
+        raise ValueError(f"{name} must have shape {list(shape)} (got {list(t.shape)})")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device} (got {t.device})")
+    return t
+
+
+def _clouds(X: torch.Tensor, Y: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    if X.device != Y.device or X.shape[0] != Y.shape[0]:
+        raise ValueError("X and Y must share device and batch size")
+    return X, Y
+
+
+def _distances(dist_xy: torch.Tensor, dist_yx: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
+    if dxy.dim() != 2:
+        raise ValueError(f"dist_xy must have shape [B, N] (got {list(dxy.shape)})")
+    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    if dyx.dim() != 2:
+        raise ValueError(f"dist_yx must have shape [B, M] (got {list(dyx.shape)})")
+    dyx = _expect(dyx, "dist_yx", torch.float32, (dxy.shape[0], dyx.shape[1]), dxy.device)
+    return dxy, dyx
+
+
+def _workspace(ws: Optional[torch.Tensor], need: int, device: torch.device) -> torch.Tensor:
+    """The caller's workspace if it is a large enough uint8 tensor on `device`,
+    else a new one."""
+    if ws is not None:
+        ws = _device_tensor(ws, "workspace", torch.uint8)
+        if ws.device != device:
+            raise ValueError(f"workspace must be on {device} (got {ws.device})")
+        if ws.numel() >= need:
+            return ws
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+
 def _stream(dev: torch.device) -> int:
     return torch.cuda.current_stream(dev).cuda_stream
 
@@ -149,9 +193,7 @@ def workspace_bytes(B: int, N: int, M: int) -> int:
 def nn_distance(X: torch.Tensor, Y: torch.Tensor, workspace: Optional[torch.Tensor] = None
                 ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
     """Nearest neighbours both ways: (dist_xy [B,N], idx_xy [B,N], dist_yx [B,M], idx_yx [B,M])."""
-    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
-    if X.device != Y.device or X.shape[0] != Y.shape[0]:
-        raise ValueError("X and Y must share device and batch size")
+    X, Y = _clouds(X, Y)
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
     dev = X.device
     dist_xy = torch.empty((B, N), dtype=torch.float32, device=dev)
@@ -159,9 +201,7 @@ def nn_distance(X: torch.Tensor, Y: torch.Tensor, workspace: Optional[torch.Tens
     dist_yx = torch.empty((B, M), dtype=torch.float32, device=dev)
     idx_yx = torch.empty((B, M), dtype=torch.int32, device=dev)
     lib = library()
-    need = int(lib.cd_workspace_bytes(B, N, M))
-    if workspace is None or workspace.numel() < need:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, int(lib.cd_workspace_bytes(B, N, M)), dev)
     with torch.cuda.device(dev):
         _check(lib.cd_forward(B, N, M, _ptr(X), _ptr(Y), _ptr(dist_xy), _ptr(idx_xy),
                               _ptr(dist_yx), _ptr(idx_yx), _ptr(workspace), workspace.numel(),
@@ -172,8 +212,7 @@ def nn_distance(X: torch.Tensor, Y: torch.Tensor, workspace: Optional[torch.Tens
 def chamfer_reduce(dist_xy: torch.Tensor, dist_yx: torch.Tensor, w1: float = 1.0,
                    w2: float = 1.0) -> torch.Tensor:
     """chamfer[b] = w1 * mean_i dist_xy[b,i] + w2 * mean_j dist_yx[b,j]."""
-    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
-    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    dxy, dyx = _distances(dist_xy, dist_yx)
     B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
     out = torch.empty(B, dtype=torch.float32, device=dxy.device)
     with torch.cuda.device(dxy.device):
@@ -184,8 +223,7 @@ def chamfer_reduce(dist_xy: torch.Tensor, dist_yx: torch.Tensor, w1: float = 1.0
 
 def f_score(dist_xy: torch.Tensor, dist_yx: torch.Tensor, tau: float):
     """F-score@tau per item: (f, precision, recall), each [B] float32."""
-    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
-    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    dxy, dyx = _distances(dist_xy, dist_yx)
     B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
     f, p, r = (torch.empty(B, dtype=torch.float32, device=dxy.device) for _ in range(3))
     with torch.cuda.device(dxy.device):
@@ -197,8 +235,7 @@ def f_score(dist_xy: torch.Tensor, dist_yx: torch.Tensor, tau: float):
 def metrics(dist_xy: torch.Tensor, dist_yx: torch.Tensor, taus, w1: float = 1.0,
             w2: float = 1.0):
     """Chamfer [B] and F-score at each tau ([ntau, B] f, precision, recall) in one launch."""
-    dxy = _device_tensor(dist_xy, "dist_xy", torch.float32)
-    dyx = _device_tensor(dist_yx, "dist_yx", torch.float32)
+    dxy, dyx = _distances(dist_xy, dist_yx)
     B, N, M = dxy.shape[0], dxy.shape[1], dyx.shape[1]
     taus = [float(t) for t in taus]
     ntau = len(taus)
@@ -222,11 +259,11 @@ def chamfer_backward(grad_out: torch.Tensor, X: torch.Tensor, Y: torch.Tensor,
                      idx_xy: torch.Tensor, idx_yx: torch.Tensor, w1: float = 1.0,
                      w2: float = 1.0) -> Tuple[torch.Tensor, torch.Tensor]:
     """Gradient of sum_b grad_out[b] * chamfer[b] w.r.t. X and Y."""
-    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
-    go = _device_tensor(grad_out, "grad_out", torch.float32)
-    ixy = _device_tensor(idx_xy, "idx_xy", torch.int32)
-    iyx = _device_tensor(idx_yx, "idx_yx", torch.int32)
+    X, Y = _clouds(X, Y)
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    go = _expect(grad_out, "grad_out", torch.float32, (B,), X.device)
+    ixy = _expect(idx_xy, "idx_xy", torch.int32, (B, N), X.device)
+    iyx = _expect(idx_yx, "idx_yx", torch.int32, (B, M), X.device)
     gX = torch.empty_like(X)
     gY = torch.empty_like(Y)
     ws = _backward_ws(B, N, M, X.device)
@@ -242,12 +279,12 @@ def chamfer_backward_pointwise(g_xy: torch.Tensor, g_yx: torch.Tensor, X: torch.
                                Y: torch.Tensor, idx_xy: torch.Tensor, idx_yx: torch.Tensor
                                ) -> Tuple[torch.Tensor, torch.Tensor]:
     """Gradient w.r.t. X and Y given dL/d dist_xy [B,N] and dL/d dist_yx [B,M]."""
-    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
-    gxy = _device_tensor(g_xy, "g_xy", torch.float32)
-    gyx = _device_tensor(g_yx, "g_yx", torch.float32)
-    ixy = _device_tensor(idx_xy, "idx_xy", torch.int32)
-    iyx = _device_tensor(idx_yx, "idx_yx", torch.int32)
+    X, Y = _clouds(X, Y)
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    gxy = _expect(g_xy, "g_xy", torch.float32, (B, N), X.device)
+    gyx = _expect(g_yx, "g_yx", torch.float32, (B, M), X.device)
+    ixy = _expect(idx_xy, "idx_xy", torch.int32, (B, N), X.device)
+    iyx = _expect(idx_yx, "idx_yx", torch.int32, (B, M), X.device)
     gX = torch.empty_like(X)
     gY = torch.empty_like(Y)
     ws = _backward_ws(B, N, M, X.device)
@@ -313,6 +350,9 @@ def mesh_sample_faces(V: torch.Tensor, F: torch.Tensor, u: torch.Tensor) -> torc
     """Area-weighted face choice fidx [B, S] for uniforms u [B, S] (Sec. 2.1)."""
     V, F = _mesh(V, F)
     u = _device_tensor(u, "u", torch.float32)
+    if u.dim() != 2:
+        raise ValueError(f"u must have shape [B, S] (got {list(u.shape)})")
+    u = _expect(u, "u", torch.float32, (V.shape[0], u.shape[1]), V.device)
     B, nv, nf, S = V.shape[0], V.shape[1], F.shape[1], u.shape[1]
     lib = library()
     ws = _mesh_ws(B, nv, nf, S, V.device)
@@ -328,9 +368,12 @@ def mesh_sample_points(V, F, fidx, r1, r2) -> torch.Tensor:
     """Reparameterised surface samples P [B, S, 3] on the faces fidx."""
     V, F = _mesh(V, F)
     fidx = _device_tensor(fidx, "fidx", torch.int32)
-    r1 = _device_tensor(r1, "r1", torch.float32)
-    r2 = _device_tensor(r2, "r2", torch.float32)
+    if fidx.dim() != 2:
+        raise ValueError(f"fidx must have shape [B, S] (got {list(fidx.shape)})")
     B, nv, nf, S = V.shape[0], V.shape[1], F.shape[1], fidx.shape[1]
+    fidx = _expect(fidx, "fidx", torch.int32, (B, S), V.device)
+    r1 = _expect(r1, "r1", torch.float32, (B, S), V.device)
+    r2 = _expect(r2, "r2", torch.float32, (B, S), V.device)
     P = torch.empty((B, S, 3), dtype=torch.float32, device=V.device)
     with torch.cuda.device(V.device):
         _check(library().cd_mesh_sample_points(B, nv, nf, _ptr(V), _ptr(F), S, _ptr(fidx), _ptr(r1),
@@ -343,10 +386,13 @@ def mesh_sample_backward(nv: int, F, fidx, r1, r2, gP) -> torch.Tensor:
     """gV [B, nv, 3]: gradient of sum(gP * P) with respect to the vertices."""
     F = _device_tensor(F, "F", torch.int32)
     fidx = _device_tensor(fidx, "fidx", torch.int32)
-    r1 = _device_tensor(r1, "r1", torch.float32)
-    r2 = _device_tensor(r2, "r2", torch.float32)
-    gP = _device_tensor(gP, "gP", torch.float32)
+    if F.dim() != 3 or F.shape[2] != 3 or fidx.dim() != 2:
+        raise ValueError("expected F [B, nf, 3] int32 and fidx [B, S] int32")
     B, nf, S = F.shape[0], F.shape[1], fidx.shape[1]
+    fidx = _expect(fidx, "fidx", torch.int32, (B, S), F.device)
+    r1 = _expect(r1, "r1", torch.float32, (B, S), F.device)
+    r2 = _expect(r2, "r2", torch.float32, (B, S), F.device)
+    gP = _expect(gP, "gP", torch.float32, (B, S, 3), F.device)
     gV = torch.empty((B, int(nv), 3), dtype=torch.float32, device=F.device)
     ws = _mesh_ws(B, int(nv), nf, S, F.device)
     with torch.cuda.device(F.device):
@@ -416,9 +462,9 @@ def p2s_forward(P, V, F):
 def p2s_backward(P, V, F, fidx, g, want_points: bool = True, want_vertices: bool = True):
     """(gP [B, S, 3] or None, gV [B, nv, 3] or None) for g [B, S] = dL/d dist."""
     P, V, F = _p2s_args(P, V, F)
-    fidx = _device_tensor(fidx, "fidx", torch.int32)
-    g = _device_tensor(g, "g", torch.float32)
     B, S, nv, nf = P.shape[0], P.shape[1], V.shape[1], F.shape[1]
+    fidx = _expect(fidx, "fidx", torch.int32, (B, S), P.device)
+    g = _expect(g, "g", torch.float32, (B, S), P.device)
     gP = torch.empty((B, S, 3), dtype=torch.float32, device=P.device) if want_points else None
     gV = torch.empty((B, nv, 3), dtype=torch.float32, device=P.device) if want_vertices else None
     ws = _p2s_ws(B, S, nv, nf, P.device)
@@ -468,13 +514,13 @@ def emd_forward(X, Y, eps_start: float = 0.5, eps_end: float = 0.01, n_iters: in
                 g_init: Optional[torch.Tensor] = None):
     """(cost [B], f [B, N], g [B, M]): approximate EMD by scheduled log-domain
     Sinkhorn iterations (the schedule and updates are documented in cd.h)."""
-    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
+    X, Y = _clouds(X, Y)
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
     f = torch.empty((B, N), dtype=torch.float32, device=X.device)
     if g_init is None:
         g = torch.empty((B, M), dtype=torch.float32, device=X.device)
     else:
-        g = _device_tensor(g_init, "g_init", torch.float32).clone()
+        g = _expect(g_init, "g_init", torch.float32, (B, M), X.device).clone()
     cost = torch.empty(B, dtype=torch.float32, device=X.device)
     ws = _emd_ws(B, N, M, X.device)
     with torch.cuda.device(X.device):
@@ -487,11 +533,11 @@ def emd_forward(X, Y, eps_start: float = 0.5, eps_end: float = 0.01, n_iters: in
 
 def emd_backward(X, Y, f, g, eps: float, grad_out):
     """(gX, gY) of sum_b grad_out[b] cost[b] with the plan held fixed."""
-    X, Y = _cloud(X, "X"), _cloud(Y, "Y")
-    f = _device_tensor(f, "f", torch.float32)
-    g = _device_tensor(g, "g", torch.float32)
-    go = _device_tensor(grad_out, "grad_out", torch.float32)
+    X, Y = _clouds(X, Y)
     B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    f = _expect(f, "f", torch.float32, (B, N), X.device)
+    g = _expect(g, "g", torch.float32, (B, M), X.device)
+    go = _expect(grad_out, "grad_out", torch.float32, (B,), X.device)
     gX = torch.empty_like(X)
     gY = torch.empty_like(Y)
     ws = _emd_ws(B, N, M, X.device)
