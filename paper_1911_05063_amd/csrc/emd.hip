@@ -15,7 +15,11 @@
 //    log-sum-exp runs in base 2 online over batches of 16 targets: the batch
 //    maximum rescales the running sum once per batch, then each pair adds
 //    exp2(z - max), z = (g_j - C_ij) log2(e) / eps.  With several target
-//    blocks the (max, sum) partials are merged by lse_merge_kernel.
+//    blocks a half-update leaves (max, sum) partials per query; the next
+//    half-update merges them for its own target block (1024 targets at a time
+//    into LDS) instead of reading finished potentials, and lse_merge_kernel
+//    merges them, with the same function, only where finished potentials are
+//    needed (the outputs).
 //  * plan_kernel: per (query block, target block) tile, either the tile's
 //    sum of P_ij C_ij (in double, reduced in a fixed order) or per query
 //    the sum of P_ij (q_i - t_j) / C_ij; partial sums over target blocks are
@@ -37,20 +41,38 @@ constexpr int kEGroup = kEQ * kEThreads;    // queries per workgroup
 constexpr int kEBatch = 16;                 // targets per online-LSE batch
 constexpr int kEMinTB = 64;                 // targets per block, at least
 constexpr int64_t kETargetTiles = 512;
+constexpr int kEChunk = 1024;               // target potentials merged into LDS at a time
 constexpr int kThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct LseArgs {
     const float *Q, *T;     // [B, nq, 3], [B, nt, 3]
-    const float *pt;        // [B, nt] potentials of the targets
+    const float *pt;        // [B, nt] potentials of the targets (finished)
+    const float2 *tpart;    // or their partials [B, tnTB, nt] from the previous half-update
     float *pq;              // [B, nq] updated potentials of the queries
     float2 *part;           // [B, nTB, nq] (max, sum) partials, base 2
     int64_t nq, nt;
     float k;                // log2(e) / eps
     float out_scale;        // -eps ln 2
     float out_bias;         // eps log(nt)  (= -eps log b)
-    int nQG, nTB, TB;
+    float t_scale, t_bias;  // out_scale, out_bias of the half-update that left tpart
+    int nQG, nTB, TB, tnTB;
 };
+
+// A finished potential from its nTB (max, sum) partials, stride apart:
+// -eps log(b sum exp(...)) = scale (M + log2 S) + bias.
+__device__ __forceinline__ float merged_potential(const float2 *p, int nTB, int64_t stride,
+                                                  float scale, float bias)
+{
+    float M = -__builtin_inff();
+    for (int t = 0; t < nTB; ++t) M = __builtin_fmaxf(M, p[static_cast<int64_t>(t) * stride].x);
+    float S = 0.0f;
+    for (int t = 0; t < nTB; ++t) {
+        const float2 v = p[static_cast<int64_t>(t) * stride];
+        S += v.y * __builtin_amdgcn_exp2f(v.x - M);
+    }
+    return __builtin_fmaf(scale, M + __log2f(S), bias);
+}
 
 __device__ __forceinline__ float dist2(float qx, float qy, float qz, float tx, float ty, float tz)
 {
@@ -84,8 +106,12 @@ __device__ __forceinline__ void lse_batch(const float (&qx)[kEQ], const float (&
     }
 }
 
+// kFromParts: the targets' potentials come as the previous half-update's
+// partials, merged here a chunk at a time into LDS.
+template <bool kFromParts>
 __global__ __launch_bounds__(kEThreads) void lse_kernel(LseArgs a)
 {
+    __shared__ float lpt[kFromParts ? kEChunk : 1];
     const int64_t per_item = static_cast<int64_t>(a.nQG) * a.nTB;
     const int64_t b = blockIdx.x / per_item;
     const int rest = static_cast<int>(blockIdx.x % per_item);
@@ -105,34 +131,47 @@ __global__ __launch_bounds__(kEThreads) void lse_kernel(LseArgs a)
     // Targets [j0, j1) of item b; 32-bit offsets within the item.
     const int j0 = tb * a.TB;
     const int j1 = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(j0) + a.TB, a.nt));
-    const int jfull = j0 + (j1 - j0) / kEBatch * kEBatch;
     const float *Tb = a.T + b * a.nt * 3;
-    const float *pb = a.pt + b * a.nt;
+    const float *pb = kFromParts ? nullptr : a.pt + b * a.nt;
     const float kk = a.k;
-    for (int jb = j0; jb < jfull; jb += kEBatch) {
-        // A full batch: contiguous wave-uniform loads, no per-target guards.
-        float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
-#pragma unroll
-        for (int u = 0; u < kEBatch; ++u) {
-            tx[u] = Tb[3 * (jb + u) + 0];
-            ty[u] = Tb[3 * (jb + u) + 1];
-            tz[u] = Tb[3 * (jb + u) + 2];
-            tk[u] = pb[jb + u] * kk;
+    // Chunks of kEChunk targets (a multiple of kEBatch, so only the last
+    // chunk has a tail); without partials the whole block is one chunk.
+    for (int c0 = j0; c0 < j1; c0 += (kFromParts ? kEChunk : j1 - j0)) {
+        const int c1 = kFromParts ? std::min(c0 + kEChunk, j1) : j1;
+        if (kFromParts) {
+            __syncthreads();  // the previous chunk is consumed
+            const float2 *tp = a.tpart + b * a.tnTB * a.nt;
+            for (int j = c0 + static_cast<int>(threadIdx.x); j < c1; j += kEThreads)
+                lpt[j - c0] = merged_potential(tp + j, a.tnTB, a.nt, a.t_scale, a.t_bias);
+            __syncthreads();
         }
-        lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
-    }
-    if (jfull < j1) {
-        // The tail: clamped loads, weight 0 past the end.
-        float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
+        auto pot = [&](int j) { return kFromParts ? lpt[j - c0] : pb[j]; };
+        const int cfull = c0 + (c1 - c0) / kEBatch * kEBatch;
+        for (int jb = c0; jb < cfull; jb += kEBatch) {
+            // A full batch: contiguous wave-uniform loads, no per-target guards.
+            float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
 #pragma unroll
-        for (int u = 0; u < kEBatch; ++u) {
-            const int j = std::min(jfull + u, j1 - 1);
-            tx[u] = Tb[3 * j + 0];
-            ty[u] = Tb[3 * j + 1];
-            tz[u] = Tb[3 * j + 2];
-            tk[u] = jfull + u < j1 ? pb[j] * kk : -__builtin_inff();
+            for (int u = 0; u < kEBatch; ++u) {
+                tx[u] = Tb[3 * (jb + u) + 0];
+                ty[u] = Tb[3 * (jb + u) + 1];
+                tz[u] = Tb[3 * (jb + u) + 2];
+                tk[u] = pot(jb + u) * kk;
+            }
+            lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
         }
-        lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
+        if (cfull < c1) {
+            // The tail: clamped loads, weight 0 past the end.
+            float tx[kEBatch], ty[kEBatch], tz[kEBatch], tk[kEBatch];
+#pragma unroll
+            for (int u = 0; u < kEBatch; ++u) {
+                const int j = std::min(cfull + u, c1 - 1);
+                tx[u] = Tb[3 * j + 0];
+                ty[u] = Tb[3 * j + 1];
+                tz[u] = Tb[3 * j + 2];
+                tk[u] = cfull + u < c1 ? pot(j) * kk : -__builtin_inff();
+            }
+            lse_batch(qx, qy, qz, m, s, tx, ty, tz, tk, kk);
+        }
     }
 #pragma unroll
     for (int k = 0; k < kEQ; ++k) {
@@ -150,15 +189,8 @@ __global__ __launch_bounds__(kThreads) void lse_merge_kernel(LseArgs a, int64_t 
     const int64_t k = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     if (k >= B * a.nq) return;
     const int64_t b = k / a.nq, q = k - b * a.nq;
-    const float2 *p = a.part + b * a.nTB * a.nq + q;
-    float M = -__builtin_inff();
-    for (int t = 0; t < a.nTB; ++t) M = __builtin_fmaxf(M, p[static_cast<int64_t>(t) * a.nq].x);
-    float S = 0.0f;
-    for (int t = 0; t < a.nTB; ++t) {
-        const float2 v = p[static_cast<int64_t>(t) * a.nq];
-        S += v.y * __builtin_amdgcn_exp2f(v.x - M);
-    }
-    a.pq[k] = __builtin_fmaf(a.out_scale, M + __log2f(S), a.out_bias);
+    a.pq[k] = merged_potential(a.part + b * a.nTB * a.nq + q, a.nTB, a.nq, a.out_scale,
+                               a.out_bias);
 }
 
 __global__ __launch_bounds__(kThreads) void fill_kernel(float *p, int64_t n, float v)
@@ -341,6 +373,7 @@ Tiles tiles_for(int64_t B, int64_t nq, int64_t nt)
 
 struct EmdLayout {
     Tiles xy, yx;               // queries X against Y; queries Y against X
+    size_t fpart_bytes;         // f's partials; g's follow (a half-update reads one, writes the other)
     size_t part_bytes, cost_bytes, grad_bytes;
 };
 
@@ -349,9 +382,10 @@ EmdLayout layout(int64_t B, int64_t N, int64_t M)
     EmdLayout L;
     L.xy = tiles_for(B, N, M);
     L.yx = tiles_for(B, M, N);
-    const size_t p1 = static_cast<size_t>(B * L.xy.nTB * N) * 8;
-    const size_t p2 = static_cast<size_t>(B * L.yx.nTB * M) * 8;
-    L.part_bytes = align256(std::max(p1, p2));
+    const size_t p1 = L.xy.nTB > 1 ? static_cast<size_t>(B * L.xy.nTB * N) * 8 : 0;
+    const size_t p2 = L.yx.nTB > 1 ? static_cast<size_t>(B * L.yx.nTB * M) * 8 : 0;
+    L.fpart_bytes = align256(p1);
+    L.part_bytes = L.fpart_bytes + align256(p2);
     L.cost_bytes = align256(static_cast<size_t>(B * L.xy.nQG * L.xy.nTB) * 8);
     const size_t g1 = L.xy.nTB > 1 ? static_cast<size_t>(B * L.xy.nTB * N) * 12 : 0;
     const size_t g2 = L.yx.nTB > 1 ? static_cast<size_t>(B * L.yx.nTB * M) * 12 : 0;
@@ -359,16 +393,31 @@ EmdLayout layout(int64_t B, int64_t N, int64_t M)
     return L;
 }
 
-hipError_t lse_pass(int64_t B, const float *Q, int64_t nq, const float *T, int64_t nt,
-                    const float *pt, float *pq, float eps, const Tiles &t, void *part,
+// The potentials of one cloud between half-updates: finished values, or the
+// (max, sum) partials a half-update left with the transform that finishes them.
+struct Potentials {
+    const float *fin = nullptr;     // [B, n], or
+    const float2 *part = nullptr;   // [B, nTB, n]
+    int nTB = 1;
+    float scale = 0.0f, bias = 0.0f;
+};
+
+// One half-update of the queries' potentials (written to pq when the targets
+// form one block, else left as partials in `part`) against the targets'.
+Potentials lse_pass(int64_t B, const float *Q, int64_t nq, const float *T, int64_t nt,
+                    const Potentials &tp, float *pq, float eps, const Tiles &t, float2 *part,
                     hipStream_t stream)
 {
     LseArgs a{};
     a.Q = Q;
     a.T = T;
-    a.pt = pt;
+    a.pt = tp.fin;
+    a.tpart = tp.part;
+    a.tnTB = tp.nTB;
+    a.t_scale = tp.scale;
+    a.t_bias = tp.bias;
     a.pq = pq;
-    a.part = static_cast<float2 *>(part);
+    a.part = part;
     a.nq = nq;
     a.nt = nt;
     a.k = kLog2e / eps;
@@ -377,11 +426,36 @@ hipError_t lse_pass(int64_t B, const float *Q, int64_t nq, const float *T, int64
     a.nQG = t.nQG;
     a.nTB = t.nTB;
     a.TB = t.TB;
-    lse_kernel<<<static_cast<uint32_t>(B * t.nQG * t.nTB), kEThreads, 0, stream>>>(a);
-    if (t.nTB > 1)
-        lse_merge_kernel<<<static_cast<uint32_t>(ceil_div(B * nq, kThreads)), kThreads, 0,
-                           stream>>>(a, B);
-    return hipGetLastError();
+    const uint32_t grid = static_cast<uint32_t>(B * t.nQG * t.nTB);
+    if (tp.fin)
+        lse_kernel<false><<<grid, kEThreads, 0, stream>>>(a);
+    else
+        lse_kernel<true><<<grid, kEThreads, 0, stream>>>(a);
+    Potentials out;
+    if (t.nTB == 1) {
+        out.fin = pq;
+    } else {
+        out.part = part;
+        out.nTB = t.nTB;
+        out.scale = a.out_scale;
+        out.bias = a.out_bias;
+    }
+    return out;
+}
+
+// Finished potentials [B, n] into `out` (a no-op if they are there already).
+void finish(int64_t B, int64_t n, const Potentials &p, float *out, hipStream_t stream)
+{
+    if (p.fin) return;
+    LseArgs a{};
+    a.part = const_cast<float2 *>(p.part);
+    a.pq = out;
+    a.nq = n;
+    a.nTB = p.nTB;
+    a.out_scale = p.scale;
+    a.out_bias = p.bias;
+    lse_merge_kernel<<<static_cast<uint32_t>(ceil_div(B * n, kThreads)), kThreads, 0, stream>>>(
+        a, B);
 }
 
 hipError_t plan_pass(int64_t B, const float *Q, int64_t nq, const float *T, int64_t nt,
@@ -438,20 +512,28 @@ hipError_t launch_emd_forward(int64_t B, int64_t N, int64_t M, const float *X, c
 {
     const EmdLayout L = layout(B, N, M);
     char *base = static_cast<char *>(ws);
-    void *part = base;
+    float2 *fpart = reinterpret_cast<float2 *>(base);
+    float2 *gpart = reinterpret_cast<float2 *>(base + L.fpart_bytes);
     double *cost_part = reinterpret_cast<double *>(base + L.part_bytes);
     if (!warm)
         fill_kernel<<<static_cast<uint32_t>(ceil_div(B * M, kThreads)), kThreads, 0, stream>>>(
             g, B * M, 0.0f);
+    Potentials pf, pg;
+    pf.fin = f;
+    pg.fin = g;
     for (int t = 0; t < n_iters; ++t) {
         const float eps = emd_eps(eps_start, eps_end, n_iters, t);
-        hipError_t e = lse_pass(B, X, N, Y, M, g, f, eps, L.xy, part, stream);
-        if (e != hipSuccess) return e;
-        e = lse_pass(B, Y, M, X, N, f, g, eps, L.yx, part, stream);
+        pf = lse_pass(B, X, N, Y, M, pg, f, eps, L.xy, fpart, stream);
+        pg = lse_pass(B, Y, M, X, N, pf, g, eps, L.yx, gpart, stream);
+        const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    finish(B, N, pf, f, stream);
+    finish(B, M, pg, g, stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     const float eps = emd_eps(eps_start, eps_end, n_iters, n_iters - 1);
-    hipError_t e = plan_pass(B, X, N, Y, M, f, g, eps, L.xy, false, nullptr, cost_part, nullptr,
+    e = plan_pass(B, X, N, Y, M, f, g, eps, L.xy, false, nullptr, cost_part, nullptr,
                              nullptr, stream);
     if (e != hipSuccess) return e;
     cost_reduce_kernel<<<static_cast<uint32_t>(B), kThreads, 0, stream>>>(
