@@ -63,6 +63,26 @@ def test_one_iteration_matches_oracle(B, N, M, eps):
     assert np.max(np.abs(g - G_or)) <= tol_g, (np.max(np.abs(g - G_or)), tol_g)
 
 
+def test_partials_merged_in_chunks_match_oracle():
+    # B*ceil(N/1024) = 512 query groups: the f-update takes Y as one block of
+    # 1100 targets, so from the second iteration on it merges the g-update's
+    # partials (Y against 2 blocks of X) for its block in two LDS chunks, the
+    # second one with a 12-target tail.  Items are independent: the oracle
+    # checks three of the 128.
+    B, N, M, iters, e0, e1 = 128, 4096, 1100, 3, 0.3, 0.1
+    print(f"[case] emd chunked partials B={B} N={N} M={M}", flush=True)
+    X, Y = synth.generate("sphere", B, N, M, 13)
+    cost, f, g = cd.emd_forward(gc.to_gpu(X), gc.to_gpu(Y), e0, e1, iters)
+    f, g = gc.to_np(f), gc.to_np(g)
+    items = [0, 63, 127]
+    _, F_or, G_or = emd_oracle.sinkhorn(X[items], Y[items], e0, e1, iters)
+    cmax = _cmax(X[items], Y[items])
+    pmax = max(np.abs(F_or).max(), np.abs(G_or).max())
+    delta = sum(_step_tol(e, max(N, M), cmax, pmax) for e in emd_oracle.schedule(e0, e1, iters)) * 2
+    assert np.max(np.abs(f[items] - F_or)) <= delta, np.max(np.abs(f[items] - F_or))
+    assert np.max(np.abs(g[items] - G_or)) <= delta, np.max(np.abs(g[items] - G_or))
+
+
 def test_full_schedule_cost_and_backward():
     B, N, M, iters, e0, e1 = 2, 1500, 1200, 40, 0.5, 0.02
     X, Y = synth.generate("sphere", B, N, M, 11)
