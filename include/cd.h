@@ -146,7 +146,8 @@ size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
  *   (CD_ERR_WORKSPACE if smaller).
  * Each term is evaluated in float32; the scatter sums are exact: every term is
  * rounded to a 64-bit fixed-point integer (grid 2^-k, with k from a bound on
- * the largest term: per block of 2048 receivers when the other cloud has at
+ * the largest term: per block of up to 2048 receivers (fewer when the clouds
+ * are small, so that more workgroups share the work) when the other cloud has at
  * most 16384 points, else per item and cloud; the grid is about 2^-61 times
  * the number of terms times that bound) and the integers are added, so the
  * result is bitwise reproducible run to run; own term + sum are added in

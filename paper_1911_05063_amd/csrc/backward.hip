@@ -21,8 +21,9 @@
 //    largest |dL/d dist|; every term component is at most 2 |g| times the
 //    box's largest extent; the grid is about 2^-61 * (cloud size) times that.
 // Either grid is far below the float32 rounding of the terms.
-//  * scatter_kernel: a workgroup owns a slice of 2048 receivers of one cloud
-//    and item and a chunk of the other cloud's senders.  Per pass of 16384
+//  * scatter_kernel: a workgroup owns a slice of up to 2048 receivers (256..2048:
+//    small problems take smaller slices, more workgroups) of one cloud and
+//    item and a chunk of the other cloud's senders.  Per pass of 16384
 //    senders it loads their neighbour indices (32 per thread, all in flight
 //    at once), queues the senders that land in its slice in LDS (a wave
 //    prefix sum and one LDS atomic per wave), and then evaluates only the
@@ -45,7 +46,9 @@ namespace {
 
 constexpr int kBlock = 512;                 // threads of a scatter workgroup
 constexpr int kSliceBits = 11;
-constexpr int kSlice = 1 << kSliceBits;     // receivers per workgroup
+constexpr int kSlice = 1 << kSliceBits;     // receivers per workgroup, at most
+constexpr int kMinSlice = 256;              // at least (small problems: more workgroups)
+constexpr int64_t kCUs = 256;
 constexpr int kIdx = 32;                    // sender indices per thread per pass
 constexpr int64_t kPass = static_cast<int64_t>(kBlock) * kIdx;   // senders per pass
 constexpr int kOwn = kSlice / kBlock;       // receivers per thread (own terms, output)
@@ -74,6 +77,7 @@ struct BwdArgs {
     int64_t B, N, M;
     float sxy, syx;     // per-item scale (w1/N, w2/M) when not pointwise
     int nblk;           // bound blocks per item (of the larger cloud)
+    int slice;          // receivers per slice (at most kSlice)
     int ns[2];          // receiving slices per item (side 0: X receives, 1: Y)
     int nc[2];          // sender chunks per item
     int local[2];       // shift from the workgroup's own terms (one chunk, one pass)
@@ -275,8 +279,8 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
     const int rest = static_cast<int>(g % (static_cast<int64_t>(ns) * nc));
     const int slice = rest / nc, c = rest % nc;
     const Side s = side_of<kPointwise>(a, side, b);
-    const int64_t r0 = static_cast<int64_t>(slice) * kSlice;
-    const int64_t r1 = std::min<int64_t>(r0 + kSlice, s.n_recv);
+    const int64_t r0 = static_cast<int64_t>(slice) * a.slice;
+    const int64_t r1 = std::min<int64_t>(r0 + a.slice, s.n_recv);
     const bool local = a.local[side] != 0;
 
     // Own terms of this thread's receivers (with one chunk; otherwise the
@@ -432,7 +436,7 @@ int64_t ceil_div(int64_t x, int64_t y) { return (x + y - 1) / y; }
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct BwdPlan {
-    int nblk;
+    int nblk, slice;
     int ns[2], nc[2], local[2];
     bool need_bound;
     int64_t chunk[2];
@@ -445,8 +449,16 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
     p.nblk = static_cast<int>(ceil_div(std::max(N, M), kBoundBlock));
     const int64_t n_recv[2] = {N, M}, n_send[2] = {M, N};
     int64_t rounds[2];
+    // Slices of kSlice receivers, halved (down to kMinSlice) while twice the
+    // workgroups still fit one per CU: every workgroup scans all senders
+    // anyway, and more of them in flight shortens the few dependent memory
+    // rounds that bound a small launch (more than one per CU measured slower).
+    p.slice = kSlice;
+    while (p.slice > kMinSlice &&
+           2 * B * (ceil_div(N, p.slice) + ceil_div(M, p.slice)) <= kCUs)
+        p.slice /= 2;
     for (int s = 0; s < 2; ++s) {
-        p.ns[s] = static_cast<int>(ceil_div(n_recv[s], kSlice));
+        p.ns[s] = static_cast<int>(ceil_div(n_recv[s], p.slice));
         rounds[s] = ceil_div(n_send[s], kPass);
     }
     // A side whose workgroups would scan many more passes than the other's
@@ -500,6 +512,7 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
     a.sxy = sxy;
     a.syx = syx;
     a.nblk = p.nblk;
+    a.slice = p.slice;
     for (int s = 0; s < 2; ++s) {
         a.ns[s] = p.ns[s];
         a.nc[s] = p.nc[s];
