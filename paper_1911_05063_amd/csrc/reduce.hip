@@ -48,8 +48,9 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
     for (int t = 0; t < (NT > 0 ? NT : 1); ++t) cp[t] = cr[t] = 0ull;
     // Groups of kGroup full strides (no bounds checks, all loads in flight;
     // unrolled by hand because loops holding ballots are not unrolled by the
-    // compiler), then single full strides, then one partial stride.  Every
-    // lane runs the same trip counts, so the ballots see the full wave.
+    // compiler), then the remaining full strides as one guarded group, then
+    // one partial stride.  Every lane runs the same trip counts, so the
+    // ballots see the full wave.
     auto take = [&](float v, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1]) {
         if (do_chamfer) sum += static_cast<double>(v);
 #pragma unroll
@@ -69,11 +70,22 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
                 for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v[u] < thr[t]));
             }
         }
-        for (; s < full; ++s) {
-            const float v = p[s * kBlock + threadIdx.x];
-            if (do_chamfer) sum += static_cast<double>(v);
+        if (s < full) {
+            // The remaining (fewer than kGroup) full strides, loads in flight
+            // together; the guard is the same for every lane.
+            float v[kGroup];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v < thr[t]));
+            for (int u = 0; u < kGroup; ++u)
+                v[u] = s + u < full ? p[(s + u) * kBlock + threadIdx.x] : 0.0f;
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                if (s + u < full) {
+                    if (do_chamfer) sum += static_cast<double>(v[u]);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v[u] < thr[t]));
+                }
+            }
+            s = full;
         }
         const int64_t i = full * kBlock + threadIdx.x;
         const bool in = i < n;
