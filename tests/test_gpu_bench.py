@@ -34,4 +34,6 @@ def test_bench_prints_one_json_line(args):
     if "roofline" in out:
         rl = out["roofline"]
         assert rl["bound"] == "alu" and rl["unit"] == "TFLOP/s" and rl["peak"] == 157.3
-        assert 0 < rl["frac"] < 1.0 and abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-9
+        # Algorithmic flops over the peak: it can pass 1 where a kernel does
+        # less work than the count credits (the fused Chamfer search), never by much.
+        assert 0 < rl["frac"] < 1.5 and abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-9
