@@ -324,3 +324,25 @@ def test_huge_batch_counts_are_rejected_without_overflow(lib):
                               None) == CD_ERR_INVALID_ARG
     assert lib.cd_mesh_sample_points(big, 3, 4, FAKE, FAKE, 2 ** 31 - 1, FAKE, FAKE, FAKE, FAKE,
                                      None) == CD_ERR_INVALID_ARG
+
+
+def test_forward_plan_bounds_over_many_shapes(lib):
+    # The workspace holds one 8-byte key per x-point and target block and per
+    # y-point and query group of 2048 x-points: its size pins the planner's
+    # block counts between those of 512-target and 32-target blocks.
+    import math
+    import random
+    rng = random.Random(5)
+    shapes = [(1, 1, 1), (1, 1024, 1024), (32, 2048, 2048), (16, 16384, 16384),
+              (4, 100000, 10000), (8, 65536, 65536), (600, 40, 50), (1, 300000, 1)]
+    shapes += [(rng.randint(1, 64), rng.randint(1, 70000), rng.randint(1, 70000)) for _ in range(300)]
+    for B, N, M in shapes:
+        ws = lib.cd_workspace_bytes(B, N, M)
+        n_qg = math.ceil(N / 2048)
+        col = 8 * B * n_qg * M
+        lo = 8 * B * math.ceil(M / 512) * N + col
+        hi = 8 * B * math.ceil(M / 32) * N + col + 512
+        assert lo <= ws <= hi, (B, N, M, ws, lo, hi)
+        assert ws % 256 == 0, (B, N, M, ws)
+        bw = lib.cd_backward_workspace_bytes(B, N, M)
+        assert bw > 0 and bw % 256 == 0, (B, N, M, bw)
