@@ -34,6 +34,7 @@ if ROOT not in sys.path:
 METRIC = "Chamfer fwd+bwd pair-evals/sec and ms/call at B=16, N=M=16384; % FP32 VALU peak"
 PEAK_FP32_TFLOPS = 157.3          # MI355X FP32 vector, 256 CU x 2.4 GHz x 256 flop/clk
 FLOPS_PER_PAIR = 9                # 3 sub + 3 mul + 2 add + 1 min per directed pair-eval
+EXECUTED_FLOPS_PER_PAIR = 10      # per computed distance: 3 sub, 3 mul, 2 add, row + column min
 # Sources of cd_forward's kernels and the flags they are built with.
 FORWARD_SOURCES = ("paper_1911_05063_amd/csrc/nn_search.hip", "paper_1911_05063_amd/build.py")
 
@@ -43,7 +44,13 @@ def parse_args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100,
-                    help="untimed steps; the GPU clock ramps up during the first ~50 ms")
+                    help="untimed steps after the settle phase")
+    ap.add_argument("--settle-ms", type=float, default=200.0,
+                    help="before the warm-up, run steps until this much GPU time has passed "
+                         "(the GPU clock ramps up over the first ~50 ms of work; reported as "
+                         "settle_ms / settle_steps)")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the per-workload figures of the five Chamfer workloads")
     ap.add_argument("--workload", type=int, default=3, help="workload number 1..5 (default 3)")
     ap.add_argument("--path", choices=("chamfer", "mesh", "p2s", "emd"), default="chamfer",
                     help="chamfer: the Chamfer step on the workload (default); mesh: the mesh "
@@ -60,6 +67,10 @@ def parse_args():
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="read two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; each with "
                          "--calib-copy 256), write profiles/traffic_mesh_b16_n16384.json, exit")
+    ap.add_argument("--ingest-valu", nargs="+", metavar="K=DIR",
+                    help="read rocprofv3 --pmc runs of SQ_INSTS_VALU, SQ_ACTIVE_INST_VALU and "
+                         "SQ_THREAD_CYCLES_VALU, one per workload k (bench.py --workload k), "
+                         "write profiles/counters_cd_forward_valu.json, exit")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="after the timed steps, fill then copy an MIB-MiB device buffer once: "
                          "reference kernels of known size for HBM-counter calibration")
@@ -102,13 +113,12 @@ def ingest_pmc(fetch_dir, write_dir, calib_mib=256):
     ref_kib = calib_mib * 1024.0
     fs = ref_kib / pick(fa, "copyBuffer")
     ws = ref_kib / pick(wa, "copyBuffer")
-    raw = {k: {"FETCH_SIZE": pick(fa, k), "WRITE_SIZE": pick(wa, k)}
-           for k in ("search_kernel", "merge_kernel")}
+    raw = {k: {"FETCH_SIZE": pick(fa, k), "WRITE_SIZE": pick(wa, k)} for k in FORWARD_KERNELS}
     fetch = sum(r["FETCH_SIZE"] for r in raw.values()) * fs * 1024.0
     write = sum(r["WRITE_SIZE"] for r in raw.values()) * ws * 1024.0
     rec = {"kernel_source_sha256": _sources_sha256(FORWARD_SOURCES),
            "workload": "mesh_b16_n16384 (B=16, N=M=16384)",
-           "launch": "cd_forward = search_kernel + merge_kernel",
+           "launch": "cd_forward = key_fill_kernel + search_kernel + merge_kernel",
            "hbm_bytes_per_launch": round(fetch + write),
            "fetch_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
            "per_kernel_kib_raw": {k: {c: round(v, 1) for c, v in r.items()} for k, r in raw.items()},
@@ -132,6 +142,88 @@ def traffic_record(kernel_sources):
     if rec.get("kernel_source_sha256") != _sources_sha256(kernel_sources):
         return None
     return rec
+
+
+VALU_RECORD = os.path.join(ROOT, "profiles", "counters_cd_forward_valu.json")
+FORWARD_KERNELS = ("key_fill_kernel", "search_kernel", "merge_kernel")
+CLOCK_GHZ, N_CU, FMA_LANES_PER_CU = 2.4, 256, 128
+
+
+def _pmc_averages(d):
+    """Per-kernel mean of each counter over the dispatches of one rocprofv3 --pmc run."""
+    import csv
+    import glob
+    from collections import defaultdict
+    paths = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not paths:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    acc = defaultdict(lambda: defaultdict(list))
+    with open(paths[0]) as f:
+        for row in csv.DictReader(f):
+            acc[row["Counter_Name"]][row["Kernel_Name"]].append(float(row["Counter_Value"]))
+    return {c: {k: sum(v) / len(v) for k, v in per.items()} for c, per in acc.items()}
+
+
+def ingest_valu(specs):
+    """VALU lane-operations per cd_forward call, per workload, from one
+    rocprofv3 --pmc run each (K=DIR: bench.py --workload K under rocprofv3)."""
+    import synth
+    rec = {"kernel_source_sha256": _sources_sha256(FORWARD_SOURCES),
+           "sources": list(FORWARD_SOURCES),
+           "counters": "SQ_INSTS_VALU, SQ_ACTIVE_INST_VALU, SQ_THREAD_CYCLES_VALU (chip totals, "
+                       "mean per dispatch)",
+           "lane_ops": "SQ_THREAD_CYCLES_VALU summed over the forward's kernels: VALU "
+                       "instructions times their active lanes",
+           "workloads": {}}
+    for spec in specs:
+        k, d = spec.split("=", 1)
+        w = synth.WORKLOADS[int(k)]
+        avg = _pmc_averages(d)
+        per = {}
+        for kern in FORWARD_KERNELS:
+            hit = {c: [v for name, v in avg[c].items() if kern in name]
+                   for c in ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_THREAD_CYCLES_VALU")}
+            if any(len(v) != 1 for v in hit.values()):
+                raise SystemExit(f"workload {k}: expected one kernel matching {kern!r}")
+            per[kern] = {c: v[0] for c, v in hit.items()}
+        lane_ops = sum(p["SQ_THREAD_CYCLES_VALU"] for p in per.values())
+        srch = per["search_kernel"]
+        rec["workloads"][w.name] = {
+            "per_kernel": per, "lane_ops_per_call": lane_ops,
+            "search_lane_utilisation": srch["SQ_THREAD_CYCLES_VALU"] / (64.0 * srch["SQ_ACTIVE_INST_VALU"]),
+            "search_valu_insts_per_computed_pair": srch["SQ_INSTS_VALU"] * 64.0 / (w.B * w.N * w.M)}
+    with open(VALU_RECORD, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
+def valu_record():
+    """The committed VALU counter record, or None when cd_forward's sources
+    changed since it was taken."""
+    if not os.path.exists(VALU_RECORD):
+        return None
+    with open(VALU_RECORD) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256") != _sources_sha256(FORWARD_SOURCES):
+        return None
+    return rec
+
+
+def forward_fractions(B, N, M, fwd_ms, rec, name):
+    """The three roofline fractions of one cd_forward call of fwd_ms:
+    credited (9 flop per directed pair-evaluation, 2 B N M of them), executed
+    (10 flop per computed distance, B N M of them: 3 sub, 1 mul, 2 FMA, the
+    row and the column minimum) and the VALU issue fraction from the counter
+    record (lane-operations over 128 lanes per CU-clock at 2.4 GHz)."""
+    t = fwd_ms * 1e-3
+    peak = PEAK_FP32_TFLOPS * 1e12
+    credited = FLOPS_PER_PAIR * 2.0 * B * N * M / t / peak
+    executed = EXECUTED_FLOPS_PER_PAIR * float(B) * N * M / t / peak
+    issue = None
+    if rec is not None and name in rec["workloads"]:
+        lane_ops = rec["workloads"][name]["lane_ops_per_call"]
+        issue = lane_ops / (t * CLOCK_GHZ * 1e9 * N_CU * FMA_LANES_PER_CU)
+    return credited, executed, issue
 
 
 def _loaded_hip_runtime():
@@ -193,20 +285,53 @@ class HipEvent:
             pass
 
 
-def timed_steps(one, n_marks, steps, warmup, stream):
-    """Warm-up, then exactly `steps` timed steps between two synchronizations.
+class Timing:
+    """Result of timed_steps: per-step events, total ms of the timed steps,
+    their wall seconds, and the settle phase (GPU ms, steps)."""
+
+    def __init__(self, events, total_ms, wall_s, settle_ms, settle_steps):
+        self.events, self.total_ms, self.wall_s = events, total_ms, wall_s
+        self.settle_ms, self.settle_steps = settle_ms, settle_steps
+
+
+def settle(one, stream, min_ms, max_wall_s=5.0):
+    """Clock settle: run steps (no events) in rounds of 5 until at least
+    min_ms of GPU time has passed between the first launch and the last
+    completion, or max_wall_s of wall time.  Returns (GPU ms, steps)."""
+    import torch
+    if min_ms <= 0:
+        return 0.0, 0
+    a, b = HipEvent(), HipEvent()
+    n, t0 = 0, time.perf_counter()
+    a.record(stream)
+    while True:
+        for _ in range(5):
+            one(None)
+        n += 5
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        if ms >= min_ms or time.perf_counter() - t0 >= max_wall_s:
+            return ms, n
+
+
+def timed_steps(one, n_marks, steps, warmup, stream, settle_ms):
+    """Settle, warm-up, then exactly `steps` timed steps between two
+    synchronizations.
 
     one(ev) runs a step and records the n_marks events of `ev` (None: no
     events).  Each recorded event costs about a microsecond of GPU time, so
-    the timed steps record only the events their figures need.  Every event
-    is created before the warm-up, so the timed steps follow the warm-up's
-    synchronization without an idle gap: after a few milliseconds idle the GPU
-    clock drops and needs tens of calls to ramp back up.  Returns (per-step
-    events, total ms, wall seconds)."""
+    the timed steps record only the events their figures need.  The GPU
+    clock ramps up over the first ~50 ms of work, so the steps first run
+    until settle_ms of GPU time has passed (settle()), then `warmup` more.
+    Every event is created before that, so the timed steps follow the
+    warm-up's synchronization without an idle gap: after a few milliseconds
+    idle the clock drops and needs tens of calls to ramp back up."""
     import torch
 
     evs = [[HipEvent() for _ in range(n_marks)] for _ in range(steps)]
     start, stop = HipEvent(), HipEvent()
+    s_ms, s_n = settle(one, stream, settle_ms)
     for _ in range(warmup):
         one(None)
     torch.cuda.synchronize()
@@ -216,7 +341,7 @@ def timed_steps(one, n_marks, steps, warmup, stream):
         one(evs[k] if n_marks else None)
     stop.record(stream)
     torch.cuda.synchronize()
-    return evs, start.elapsed_time(stop), time.perf_counter() - t0
+    return Timing(evs, start.elapsed_time(stop), time.perf_counter() - t0, s_ms, s_n)
 
 
 class Step:
@@ -294,26 +419,59 @@ def repeat_for(run_once, seconds):
             return reps, dt
 
 
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def time_cpu_oracle(X, Y, taus, items, seconds):
     """The CPU oracle (as it stands) on `items` batch items of the workload:
     nearest neighbours both ways, Chamfer, F-score at each tau, backward;
-    repeated for about `seconds`."""
+    repeated for about `seconds` with all of the oracle's threads, then on
+    one item with one thread for about half as long."""
     import numpy as np
     import oracle
-    Xs, Ys = X[:items], Y[:items]
-    oracle.nn_one_way(Xs[:, :8], Ys[:, :8])  # load + spin up the thread pool
+    oracle.nn_one_way(X[:1, :8], Y[:1, :8])  # load + spin up the thread pool
 
-    def once():
-        r = oracle.forward_all(Xs, Ys, taus)
-        oracle.backward(np.ones(items), Xs, Ys, r["idx_xy"], r["idx_yx"])
+    def leg(n_items, secs):
+        Xs, Ys = X[:n_items], Y[:n_items]
 
-    reps, dt = repeat_for(once, seconds)
-    pairs = 2.0 * items * X.shape[1] * Y.shape[1] * reps
-    return {"value": pairs / dt, "unit": "pair-evals/s", "cores": oracle.threads(),
-            "kind": "oracle", "seconds": round(dt, 3),
+        def once():
+            r = oracle.forward_all(Xs, Ys, taus)
+            oracle.backward(np.ones(n_items), Xs, Ys, r["idx_xy"], r["idx_yx"])
+
+        reps, dt = repeat_for(once, secs)
+        return 2.0 * n_items * X.shape[1] * Y.shape[1] * reps / dt, reps, dt
+
+    what = (f"float32 nearest neighbours both ways, Chamfer, F-score at {len(taus)} thresholds "
+            f"and backward")
+    threads = oracle.threads()
+    rate, reps, dt = leg(items, seconds)
+    oracle.set_threads(1)
+    try:
+        rate1, reps1, dt1 = leg(1, seconds / 2)
+    finally:
+        oracle.set_threads(threads)
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
+    return {"value": rate, "unit": "pair-evals/s", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 3), "cpu_model": cpu_model(),
+            "host_cpus": os.cpu_count(), "cpus_available": affinity,
             "sample": (f"{items} of {X.shape[0]} batch items (N={X.shape[1]}, M={Y.shape[1]}), "
-                       f"{reps} times: float32 nearest neighbours both ways, Chamfer, F-score at "
-                       f"{len(taus)} thresholds and backward, OpenMP over queries")}
+                       f"{reps} times: {what}, OpenMP over queries ({threads} threads)"),
+            "single_thread": {"value": rate1, "unit": "pair-evals/s", "cores": 1,
+                              "seconds": round(dt1, 3),
+                              "sample": f"1 batch item (N={X.shape[1]}, M={Y.shape[1]}), "
+                                        f"{reps1} times: {what}, one thread"}}
 
 
 def mesh_step_bench(args):
@@ -366,10 +524,11 @@ def mesh_step_bench(args):
         if ev is not None:
             ev[3].record(stream)
 
-    _, total_ms, _ = timed_steps(one, 0, args.steps, args.warmup, stream)
-    ms = total_ms / args.steps
+    tm = timed_steps(one, 0, args.steps, args.warmup, stream, args.settle_ms)
+    ms = tm.total_ms / args.steps
     nb = min(args.steps, 50)
-    evs, _, _ = timed_steps(one, 4, nb, args.warmup, stream)  # per-call breakdown, after the timed steps
+    # per-call breakdown, after the timed steps
+    evs = timed_steps(one, 4, nb, args.warmup, stream, args.settle_ms / 4).events
     samp = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
     cham = statistics.mean(e[1].elapsed_time(e[2]) for e in evs)
     sbwd = statistics.mean(e[2].elapsed_time(e[3]) for e in evs)
@@ -378,6 +537,7 @@ def mesh_step_bench(args):
                      "sampling bwd)",
            "value": pairs / (ms * 1e-3), "unit": "pair-evals/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
            "config": {"workload": "mesh_sampling_b16_t200_s16384", "B": B, "triangles": T,
@@ -461,9 +621,9 @@ def p2s_step_bench(args):
 
     print(f"[bench] {w.name}: B={B} S={S} nv={nv} nf={nf} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    evs, total_ms, _ = timed_steps(one, 2, args.steps, args.warmup, stream)
-    ms = total_ms / args.steps
-    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
+    tm = timed_steps(one, 2, args.steps, args.warmup, stream, args.settle_ms)
+    ms = tm.total_ms / args.steps
+    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in tm.events)
     rest = ms - fwd
     pairs = float(B) * S * nf
     achieved = P2S_FLOPS_PER_PAIR * pairs / (fwd * 1e-3) / 1e12
@@ -471,6 +631,7 @@ def p2s_step_bench(args):
                      "(forward + mean + backward to points and vertices)",
            "value": pairs / (ms * 1e-3), "unit": "point-triangle pair-evals/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
            "config": {"workload": w.name, "B": B, "S": S, "nv": nv, "nf": nf},
@@ -555,9 +716,9 @@ def emd_step_bench(args):
 
     print(f"[bench] emd on {w.describe()} iters={EMD_ITERS} eps={EMD_EPS} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    evs, total_ms, _ = timed_steps(one, 2, args.steps, args.warmup, stream)
-    ms = total_ms / args.steps
-    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in evs)
+    tm = timed_steps(one, 2, args.steps, args.warmup, stream, args.settle_ms)
+    ms = tm.total_ms / args.steps
+    fwd = statistics.mean(e[0].elapsed_time(e[1]) for e in tm.events)
     bwd = ms - fwd
     pairs = float(B) * N * M * (2 * EMD_ITERS + 3)
     lse_pairs = float(B) * N * M * 2 * EMD_ITERS
@@ -567,6 +728,7 @@ def emd_step_bench(args):
     out = {"metric": "approximate-EMD step Sinkhorn pair-evals/sec (50 iterations + cost + backward)",
            "value": pairs / (ms * 1e-3), "unit": "Sinkhorn pair-evals/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
            "config": {"workload": w.name, "B": B, "N": N, "M": M, "iters": EMD_ITERS,
@@ -587,6 +749,9 @@ def main():
     if args.ingest_pmc:
         ingest_pmc(*args.ingest_pmc)
         return
+    if args.ingest_valu:
+        ingest_valu(args.ingest_valu)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the batch items are independent: shard them across GPUs).", file=sys.stderr)
@@ -600,19 +765,27 @@ def main():
     if args.path == "mesh":
         mesh_step_bench(args)
         return
-    import numpy as np
+    chamfer_bench(args)
+
+
+def chamfer_step_on(k):
+    """Workload k's clouds on cuda:0 and a Step over them (inputs resident in HBM)."""
     import torch
     import synth
-
-    w = synth.WORKLOADS[args.workload]
-    X_np, Y_np = synth.workload(args.workload)
+    X_np, Y_np = synth.workload(k)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    X = torch.from_numpy(X_np).to(dev)
-    Y = torch.from_numpy(Y_np).to(dev)
-    step = Step(X, Y, w.taus)
-    print(f"[bench] {w.describe()} steps={args.steps} warmup={args.warmup}", file=sys.stderr,
-          flush=True)
+    step = Step(torch.from_numpy(X_np).to(dev), torch.from_numpy(Y_np).to(dev),
+                synth.WORKLOADS[k].taus)
+    return step, X_np, Y_np
+
+
+def measure_chamfer(step, steps, warmup, settle_ms, breakdown_steps):
+    """The Chamfer step (cd_forward, cd_metrics, cd_backward) timed: `steps`
+    steps with events around every cd_forward (the roofline's launch
+    duration), then a pass of breakdown_steps with four events per step for
+    the metrics and backward calls (its own settle: the clock drops while
+    its events are created)."""
 
     def one_step(ev=None):
         if ev is not None:
@@ -627,15 +800,61 @@ def main():
         if ev is not None and len(ev) > 2:
             ev[3].record(step.stream)
 
-    # The timed steps record the two events around cd_forward (the roofline's
-    # launch duration); a short pass after them (its own warm-up: the GPU
-    # clock drops while its events are created) times metrics and backward.
-    evs, total_ms, wall = timed_steps(one_step, 2, args.steps, args.warmup, step.stream)
-    fwd = [e[0].elapsed_time(e[1]) for e in evs]
-    nb = min(args.steps, 50)
-    bd, _, _ = timed_steps(one_step, 4, nb, args.warmup, step.stream)
-    red = [e[1].elapsed_time(e[2]) for e in bd]
-    bwd = [e[2].elapsed_time(e[3]) for e in bd]
+    tm = timed_steps(one_step, 2, steps, warmup, step.stream, settle_ms)
+    bd = timed_steps(one_step, 4, breakdown_steps, warmup, step.stream, settle_ms / 4)
+    return {"timing": tm, "ms_per_step": tm.total_ms / steps,
+            "fwd": [e[0].elapsed_time(e[1]) for e in tm.events],
+            "red": [e[1].elapsed_time(e[2]) for e in bd.events],
+            "bwd": [e[2].elapsed_time(e[3]) for e in bd.events]}
+
+
+def config_figures(w, m, rec):
+    """Per-workload figures of one measure_chamfer() result."""
+    fwd = statistics.mean(m["fwd"])
+    credited, executed, issue = forward_fractions(w.B, w.N, w.M, fwd, rec, w.name)
+    return {"B": w.B, "N": w.N, "M": w.M, "steps": len(m["timing"].events),
+            "ms_per_step": m["ms_per_step"],
+            "pair_evals_per_s": 2.0 * w.B * w.N * w.M / (m["ms_per_step"] * 1e-3),
+            "ms_per_call": {"forward": fwd, "metrics": statistics.mean(m["red"]),
+                            "backward": statistics.mean(m["bwd"])},
+            "frac": credited, "executed_frac": executed, "valu_issue_frac": issue}
+
+
+def per_config(args, main_k, main_fig, rec):
+    """Every Chamfer workload's figures (GPU only), about 50 ms of timed
+    steps each; the benchmark's own workload reuses its main figures."""
+    import torch
+    import synth
+    out = {}
+    for k in sorted(synth.WORKLOADS):
+        w = synth.WORKLOADS[k]
+        if k == main_k:
+            out[w.name] = main_fig
+            continue
+        step, _, _ = chamfer_step_on(k)
+        probe_ms, probe_n = settle(lambda ev=None: (step.forward(), step.reduce_fscore(),
+                                                    step.backward()),
+                                   step.stream, 100.0)
+        n = int(min(200, max(10, 50.0 / (probe_ms / probe_n))))
+        print(f"[bench] per-config {w.name}: {n} steps", file=sys.stderr, flush=True)
+        m = measure_chamfer(step, n, 5, 20.0, min(n, 50))
+        out[w.name] = config_figures(w, m, rec)
+        del step
+        torch.cuda.empty_cache()
+    return out
+
+
+def chamfer_bench(args):
+    import torch
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    step, X_np, Y_np = chamfer_step_on(args.workload)
+    dev = step.X.device
+    print(f"[bench] {w.describe()} steps={args.steps} warmup={args.warmup} "
+          f"settle_ms={args.settle_ms}", file=sys.stderr, flush=True)
+    m = measure_chamfer(step, args.steps, args.warmup, args.settle_ms, min(args.steps, 50))
+    tm, fwd, red, bwd = m["timing"], m["fwd"], m["red"], m["bwd"]
 
     if args.calib_copy > 0:
         n = args.calib_copy * (1 << 20) // 4
@@ -649,10 +868,12 @@ def main():
 
     B, N, M = w.B, w.N, w.M
     pairs = 2.0 * B * N * M
-    ms_per_step = total_ms / args.steps
+    ms_per_step = m["ms_per_step"]
     value = pairs / (ms_per_step * 1e-3)
     fwd_avg_s = statistics.mean(fwd) * 1e-3
     achieved = FLOPS_PER_PAIR * pairs / fwd_avg_s / 1e12
+    rec = valu_record()
+    main_fig = config_figures(w, m, rec)
     out = {
         "metric": METRIC,
         "value": value,
@@ -661,6 +882,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "settle_ms": tm.settle_ms,
+        "settle_steps": tm.settle_steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -670,18 +893,30 @@ def main():
                    "taus": list(w.taus), "seed": w.seed},
         "ms_per_call": {"forward": statistics.mean(fwd), "forward_median": statistics.median(fwd),
                         "reduce_fscore": statistics.mean(red), "backward": statistics.mean(bwd),
-                        "fwd_bwd": ms_per_step, "breakdown_steps": nb},
+                        "fwd_bwd": ms_per_step, "breakdown_steps": len(red)},
         "pct_fp32_valu_peak": 100.0 * FLOPS_PER_PAIR * value / (PEAK_FP32_TFLOPS * 1e12),
-        "wall_s": wall,
-        "roofline": {"bound": "alu", "kernel": "cd_forward (search_kernel + merge_kernel)",
+        "wall_s": tm.wall_s,
+        "roofline": {"bound": "alu",
+                     "kernel": "cd_forward (key_fill_kernel + search_kernel + merge_kernel)",
                      "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+                     "executed_frac": main_fig["executed_frac"],
+                     "valu_issue_frac": main_fig["valu_issue_frac"],
+                     "frac_note": "frac credits 9 flop per directed pair-evaluation (2 B N M); "
+                                  "executed_frac counts the 10 flop per distance the fused "
+                                  "kernel computes (B N M); valu_issue_frac is VALU "
+                                  "lane-operations (counter record) over 128 lanes per "
+                                  "CU-clock at 2.4 GHz",
                      "algorithmic_bytes": 12.0 * B * (N + M) + 8.0 * B * (N + M),
                      "work_per_launch": f"{FLOPS_PER_PAIR} flop x {pairs:.4g} directed pair-evals"},
     }
     tr = traffic_record(FORWARD_SOURCES) if args.workload == 3 else None
     if tr is not None:
         out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
+    if not args.no_per_config:
+        del step
+        torch.cuda.empty_cache()
+        out["per_config"] = per_config(args, args.workload, main_fig, rec)
     if not args.no_cpu_baseline:
         items = args.cpu_items if args.cpu_items > 0 else B
         print(f"[bench] CPU oracle baseline on {items} item(s)", file=sys.stderr, flush=True)

@@ -63,8 +63,9 @@ const char *cd_last_error(void);
 const char *cd_version(void);
 
 /*
- * Bytes of device workspace cd_forward needs for this shape (0 when B == 0).
- * Returns 0 and sets cd_last_error() for an invalid shape.
+ * Bytes of device workspace cd_forward needs for this shape (0 when B == 0):
+ * one 8-byte key per point of both clouds, 8 B (N + M) rounded up to 256-byte
+ * segments.  Returns 0 and sets cd_last_error() for an invalid shape.
  */
 size_t cd_workspace_bytes(int64_t B, int64_t N, int64_t M);
 

@@ -67,6 +67,7 @@ def _load():
     lib = ctypes.CDLL(LIB_PATH)
     i64, f32p, f64p = ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p
     lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
     lib.oracle_nn.argtypes = [i64, i64, i64, f32p, f32p, ctypes.c_int, f32p, f32p]
     lib.oracle_chamfer.argtypes = [i64, i64, i64, f32p, f32p, ctypes.c_double, ctypes.c_double, f64p]
     lib.oracle_fscore.argtypes = [i64, i64, i64, f32p, f32p, ctypes.c_float, f64p, f64p, f64p,
@@ -99,6 +100,12 @@ def _cloud(a) -> np.ndarray:
 def threads() -> int:
     """OpenMP threads the oracle's nearest-neighbour loop uses."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for the oracle's later parallel loops (timing only: results do
+    not depend on the thread count)."""
+    _load().oracle_set_threads(int(n))
 
 
 def nn_one_way(P, Q, fused: bool = False) -> Tuple[np.ndarray, np.ndarray]:

@@ -52,6 +52,16 @@ int oracle_threads(void)
 #endif
 }
 
+/* Threads of later parallel loops (timing only; the results do not depend on it). */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Nearest neighbour of every query p in P[b] among the targets Q[b].
  * P: [B, NP, 3], Q: [B, NQ, 3] float32 row-major.  dist/idx: [B, NP].

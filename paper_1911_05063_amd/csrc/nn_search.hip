@@ -29,9 +29,13 @@
 //    so that the final round is filled with short tiles.  A problem too small
 //    for one round gets blocks of 32..512 targets, about half a round of
 //    tiles.
-//  * Each tile writes one packed (distance, batch start) key per x-point and
-//    one (distance, lane) key per y-point to the workspace; a merge kernel
-//    takes the minimum key over tiles and recovers the exact lowest index by
+//  * Each tile folds its packed (distance, batch start) key per x-point and
+//    (distance, lane) key per y-point into one key per point in the workspace
+//    with a 64-bit global atomicMin (the arrays are filled with ~0 first), so
+//    the workspace is 8 B (N + M) bytes whatever the tiling.  Distances are
+//    >= +0, so the unsigned key order is distance first, then batch (lane):
+//    the minimum names the first batch (lowest lane) that reaches the minimum
+//    distance.  A merge kernel then recovers the exact lowest index by
 //    recomputing the kBatch candidate targets of a row (8 lanes per x-point)
 //    or the kQ candidate x-points of a column with the same instructions, so
 //    equality is exact.
@@ -88,8 +92,8 @@ __device__ __forceinline__ unsigned long long pack_key(float d, uint32_t low)
 struct KernelArgs {
     const float *X;
     const float *Y;
-    unsigned long long *rowpart;  // [B, nTB, N]  (distance, batch start) per x-point and block
-    unsigned long long *colpart;  // [B, nQG, M]  (distance, x lane) per y-point and group
+    unsigned long long *rowkey;  // [B, N]  min (distance, batch start) per x-point
+    unsigned long long *colkey;  // [B, M]  min (distance, x lane) per y-point
     int32_t N, M, nQG, nTB, TB;
     int32_t TS, nBig;   // small blocks of TS targets follow nBig blocks of TB
     int32_t pad;
@@ -247,13 +251,40 @@ void search_kernel(KernelArgs a)
     if (j < t1)
         search_batch<false>(Yb, j, t1, qx, qy, qz, best, bsub, lds, lane, colkeys, t0, lane0);
 
-    unsigned long long *rp = a.rowpart + (static_cast<int64_t>(b) * a.nTB + tb) * a.N;
+    // Rows: this wave's kWave*kQ keys go through its LDS buffer (free after the
+    // last batch; a wave's LDS operations execute in order) so that
+    // consecutive lanes update consecutive x-points: 512 contiguous bytes per
+    // atomic instruction instead of a 64-byte stride.
+    unsigned long long *kl = reinterpret_cast<unsigned long long *>(lds);
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int k = 0; k < kQ; ++k)
-        if (xbase + k < nx) rp[xbase + k] = pack_key(best[k], static_cast<uint32_t>(bsub[k]));
+        kl[lane * kQ + k] = pack_key(best[k], static_cast<uint32_t>(bsub[k]));
+    __builtin_amdgcn_wave_barrier();
+    unsigned long long *rp = a.rowkey + static_cast<int64_t>(b) * a.N;
+    const uint32_t wx = lane0 * kQ;
+#pragma unroll
+    for (int k = 0; k < kQ; ++k) {
+        const uint32_t p = k * kWave + lane;
+        if (wx + p < nx) atomicMin(rp + wx + p, kl[p]);
+    }
     __syncthreads();
-    unsigned long long *cp = a.colpart + (static_cast<int64_t>(b) * a.nQG + qg) * a.M;
-    for (int t = threadIdx.x; t < t1 - t0; t += kThreads) cp[t0 + t] = colkeys[t];
+    unsigned long long *cp = a.colkey + static_cast<int64_t>(b) * a.M;
+    for (int t = threadIdx.x; t < t1 - t0; t += kThreads) atomicMin(cp + t0 + t, colkeys[t]);
+}
+
+// Every key of the workspace to ~0 (no key yet), before the search folds in
+// its tiles.  A kernel rather than a memset, so that callers may capture the
+// forward in a graph.
+constexpr int kFillThreads = 256;
+constexpr int64_t kFillBlocks = 2048;
+
+__global__ __launch_bounds__(kFillThreads) void key_fill_kernel(unsigned long long *k, int64_t n)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kFillThreads;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kFillThreads + threadIdx.x; i < n;
+         i += stride)
+        k[i] = ~0ull;
 }
 
 // One point's coordinates: 12-byte loads (dword-aligned vector loads).
@@ -268,12 +299,12 @@ __host__ __device__ __forceinline__ int64_t merge_row_threads(int64_t nx)
 }
 
 // Rows first (threads [0, merge_row_threads(B*N))), then one thread per
-// column.  A wave of rows takes the minimum key of its 64 x-points (one per
-// lane), then rescans their candidate batches 8 x-points at a time: 8 lanes
+// column.  A wave of rows reads the keys of its 64 x-points (one per lane),
+// then rescans their candidate batches 8 x-points at a time: 8 lanes
 // per x-point, each lane 4 consecutive targets (48 contiguous bytes), and the
 // lowest matching index over the 8 lanes.  The rescan loads are clamped into
 // the cloud instead of guarded, so that two rounds' loads are in flight
-// together.  The partial keys are read once: non-temporal loads keep them
+// together.  The keys are read once: non-temporal loads keep them
 // from evicting the coordinates that the rescans read.
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
@@ -293,11 +324,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
         if (mine) {
             const int64_t b = t / a.N, i = t - b * a.N;
             bi = static_cast<int>(b);
-            const unsigned long long *rp = a.rowpart + b * a.nTB * static_cast<int64_t>(a.N) + i;
-            unsigned long long key = ~0ull;
-#pragma unroll 8
-            for (int tb = 0; tb < a.nTB; ++tb)
-                key = min(key, __builtin_nontemporal_load(rp + static_cast<int64_t>(tb) * a.N));
+            const unsigned long long key = __builtin_nontemporal_load(a.rowkey + b * a.N + i);
             val = __uint_as_float(static_cast<uint32_t>(key >> 32));
             js = static_cast<int>(static_cast<uint32_t>(key));
             js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
@@ -358,11 +385,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
     } else {
         const int64_t u = t - nr;
         const int64_t b = u / a.M, jy = u - b * a.M;
-        const unsigned long long *cp = a.colpart + b * a.nQG * static_cast<int64_t>(a.M) + jy;
-        unsigned long long key = ~0ull;
-#pragma unroll 8
-        for (int q = 0; q < a.nQG; ++q)
-            key = min(key, __builtin_nontemporal_load(cp + static_cast<int64_t>(q) * a.M));
+        const unsigned long long key = __builtin_nontemporal_load(a.colkey + b * a.M + jy);
         const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
         // Candidates: the kQ x-points of the winning lane, as a fixed-length,
         // fully unrolled scan (indices clamped to the last one) so that all
@@ -387,16 +410,16 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct WsOffsets {
-    size_t rowpart, colpart, total;
+    size_t rowkey, colkey, total;
 };
 
 WsOffsets ws_offsets(const FwdPlan &p)
 {
     auto up = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
     WsOffsets w;
-    w.rowpart = 0;
-    w.colpart = up(static_cast<size_t>(p.B) * p.nTB * p.N * 8);
-    w.total = w.colpart + up(static_cast<size_t>(p.B) * p.nQG * p.M * 8);
+    w.rowkey = 0;
+    w.colkey = up(static_cast<size_t>(p.B) * p.N * 8);
+    w.total = w.colkey + up(static_cast<size_t>(p.B) * p.M * 8);
     return w;
 }
 
@@ -462,8 +485,8 @@ hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream
     KernelArgs a;
     a.X = f.X;
     a.Y = f.Y;
-    a.rowpart = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.rowpart);
-    a.colpart = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.colpart);
+    a.rowkey = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.rowkey);
+    a.colkey = reinterpret_cast<unsigned long long *>(static_cast<char *>(f.ws) + w.colkey);
     a.N = p.N;
     a.M = p.M;
     a.nQG = p.nQG;
@@ -473,6 +496,10 @@ hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream
     a.nBig = p.nBig;
     a.pad = 0;
     a.B = p.B;
+    // The two key arrays and the padding between them: one fill.
+    const int64_t nkeys = static_cast<int64_t>(w.total / 8);
+    key_fill_kernel<<<static_cast<uint32_t>(std::min(ceil_div(nkeys, kFillThreads), kFillBlocks)),
+                      kFillThreads, 0, stream>>>(a.rowkey, nkeys);
     search_kernel<<<static_cast<uint32_t>(forward_tiles(p)), kThreads, 0, stream>>>(a);
     const int64_t total = merge_row_threads(p.B * static_cast<int64_t>(p.N)) + p.B * p.M;
     merge_kernel<<<static_cast<uint32_t>(ceil_div(total, kMergeThreads)), kMergeThreads, 0,

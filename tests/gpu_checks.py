@@ -43,6 +43,9 @@ def gpu_forward(X: np.ndarray, Y: np.ndarray):
 
 def assert_nn_bitwise(gpu, ref, what=""):
     names = ("dist_xy", "idx_xy", "dist_yx", "idx_yx")
+    # No index is -1 (no neighbour found) for finite inputs within range.
+    for n, g in zip(names[1::2], gpu[1::2]):
+        assert g.size == 0 or g.min() >= 0, f"{what} {n}: an index is negative"
     for n, g, r in zip(names, gpu, ref):
         if not np.array_equal(g, r):
             bad = np.argwhere(g != r)

@@ -326,23 +326,21 @@ def test_huge_batch_counts_are_rejected_without_overflow(lib):
                                      None) == CD_ERR_INVALID_ARG
 
 
-def test_forward_plan_bounds_over_many_shapes(lib):
-    # The workspace holds one 8-byte key per x-point and target block and per
-    # y-point and query group of 2048 x-points: its size pins the planner's
-    # block counts between those of 512-target and 32-target blocks.
-    import math
+def test_forward_workspace_is_linear_in_the_clouds(lib):
+    # The forward keeps one 8-byte key per point of each cloud (tiles fold
+    # into them with atomic minima), whatever the planner's tiling: 8 B N and
+    # 8 B M bytes, each rounded up to 256.  The backward's workspace is
+    # nonzero and aligned for the same shapes.
     import random
     rng = random.Random(5)
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
     shapes = [(1, 1, 1), (1, 1024, 1024), (32, 2048, 2048), (16, 16384, 16384),
-              (4, 100000, 10000), (8, 65536, 65536), (600, 40, 50), (1, 300000, 1)]
+              (4, 100000, 10000), (8, 65536, 65536), (600, 40, 50), (1, 300000, 1),
+              (1, 2 ** 20, 2 ** 20), (1, 2 ** 22, 2 ** 22), (1, 2 ** 30, 2 ** 30)]
     shapes += [(rng.randint(1, 64), rng.randint(1, 70000), rng.randint(1, 70000)) for _ in range(300)]
     for B, N, M in shapes:
         ws = lib.cd_workspace_bytes(B, N, M)
-        n_qg = math.ceil(N / 2048)
-        col = 8 * B * n_qg * M
-        lo = 8 * B * math.ceil(M / 512) * N + col
-        hi = 8 * B * math.ceil(M / 32) * N + col + 512
-        assert lo <= ws <= hi, (B, N, M, ws, lo, hi)
-        assert ws % 256 == 0, (B, N, M, ws)
+        assert ws == up(8 * B * N) + up(8 * B * M), (B, N, M, ws)
+        assert ws <= 8 * B * (N + M) + 512
         bw = lib.cd_backward_workspace_bytes(B, N, M)
         assert bw > 0 and bw % 256 == 0, (B, N, M, bw)

@@ -1,8 +1,10 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Small and medium cases are compared element by element; the five full-size
-workloads are compared on sampled queries the oracle computes one by one,
-on the whole-array reductions, and on closed forms that hold at any size.
+Small and medium cases are compared element by element; so are the five
+full-size workloads (every row of both directions, against the oracle in the
+kernel's precision bitwise and against the separately rounded oracle under the
+near-tie rule), together with the whole-array reductions; a pair of
+million-point clouds is checked against closed forms and sampled oracle rows.
 """
 import os
 
@@ -401,9 +403,11 @@ def _sample_rows(rng, B, n, count):
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_full_size_workload(k):
     """Workload k at its full size, in the launch configuration the benchmark
-    times: sampled queries against the oracle (bitwise, same precision),
-    whole-array Chamfer / F-score / gradients against the oracle fed the
-    GPU's own neighbours, and the gradient identities."""
+    times: every distance and index of both directions against the oracle
+    (bitwise in the kernel's precision; under the near-tie rule against the
+    separately rounded order), whole-array Chamfer / F-score / gradients
+    against the oracle fed the GPU's own neighbours, and the gradient
+    identities."""
     w = synth.WORKLOADS[k]
     print(f"[full] {w.describe()}", flush=True)
     X, Y = synth.workload(k)
@@ -415,15 +419,14 @@ def test_full_size_workload(k):
     fs = {t: cd.f_score(dxy, dyx, t) for t in w.taus}
     mch, mf, mp, mr = cd.metrics(dxy, dyx, w.taus)
     torch.cuda.synchronize()
-    dxy_n, ixy_n, dyx_n, iyx_n = (gc.to_np(t) for t in (dxy, ixy, dyx, iyx))
-    rng = np.random.default_rng(1000 + k)
-    count = 1024 if k != 5 else 384
-    for P, Q, dist, idx, n in ((X, Y, dxy_n, ixy_n, w.N), (Y, X, dyx_n, iyx_n, w.M)):
-        rows = _sample_rows(rng, w.B, n, count)
-        rd, ri = gc.sample_nn(P, Q, rows, fused=True)
-        assert np.array_equal(dist[rows[:, 0], rows[:, 1]], rd)
-        assert np.array_equal(idx[rows[:, 0], rows[:, 1]], ri)
+    got = tuple(gc.to_np(t) for t in (dxy, ixy, dyx, iyx))
+    dxy_n, ixy_n, dyx_n, iyx_n = got
     assert ixy_n.min() >= 0 and ixy_n.max() < w.M and iyx_n.min() >= 0 and iyx_n.max() < w.N
+    gc.assert_nn_bitwise(got, oracle.nn(X, Y, fused=True), f"workload {k}")
+    ref = oracle.nn(X, Y, fused=False)
+    gc.assert_nn_unfused(X, Y, dxy_n, ixy_n, ref[0], ref[1])
+    gc.assert_nn_unfused(Y, X, dyx_n, iyx_n, ref[2], ref[3])
+    del ref
     gc.assert_chamfer(gc.to_np(ch), dxy_n, dyx_n)
     assert np.array_equal(gc.to_np(mch), gc.to_np(ch))
     for ti, (t, (f, p, r)) in enumerate(fs.items()):
@@ -465,6 +468,41 @@ def test_lattice_closed_form_full_size(B, dims):
     assert np.array_equal(gc.to_np(gX), np.broadcast_to((-k * s).astype(np.float32), X.shape))
     assert np.array_equal(gc.to_np(gY), np.broadcast_to((k * s).astype(np.float32), Y.shape))
     assert np.all(gc.to_np(f) == 1.0)
+
+
+def test_million_point_clouds_in_a_linear_workspace():
+    """B = 1, N = M = 2^20 (a 128 x 128 x 64 dyadic lattice and its permuted
+    shifted copy): the forward's workspace is one key per point (16 MiB, far
+    under 1 GB), every distance, index and gradient equals its closed form
+    bitwise, and sampled rows equal the oracle's in the kernel's precision."""
+    h, s = 1.0 / 16, np.array([1 / 64, -3 / 256, 1 / 128])
+    X, Y, perm = synth.lattice_pair(1, (128, 128, 64), h, s, seed=78)
+    N = X.shape[1]
+    assert N == 2 ** 20
+    ws = cd.workspace_bytes(1, N, N)
+    assert ws == 16 * N and ws <= 1 << 30
+    print(f"[million] N = M = {N}, workspace {ws} bytes", flush=True)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    gX, gY = cd.chamfer_backward(torch.ones(1, device="cuda:0"), Xg, Yg, ixy, iyx)
+    torch.cuda.synchronize()
+    s2 = np.float32((s ** 2).sum())
+    assert bool((dxy == float(s2)).all()) and bool((dyx == float(s2)).all())
+    assert np.array_equal(gc.to_np(ixy)[0], perm[0])
+    inv = np.empty_like(perm[0])
+    inv[perm[0]] = np.arange(N)
+    assert np.array_equal(gc.to_np(iyx)[0], inv)
+    k = 2.0 * (2.0 / N)
+    assert bool((gX == torch.tensor((-k * s).astype(np.float32), device="cuda:0")).all())
+    assert bool((gY == torch.tensor((k * s).astype(np.float32), device="cuda:0")).all())
+    rng = np.random.default_rng(79)
+    for P, Q, dist, idx in ((X, Y, dxy, ixy), (Y, X, dyx, iyx)):
+        rows = _sample_rows(rng, 1, N, 256)
+        rd, ri = gc.sample_nn(P, Q, rows, fused=True)
+        assert np.array_equal(gc.to_np(dist)[rows[:, 0], rows[:, 1]], rd)
+        assert np.array_equal(gc.to_np(idx)[rows[:, 0], rows[:, 1]], ri)
+    del Xg, Yg, dxy, ixy, dyx, iyx, gX, gY
+    torch.cuda.empty_cache()
 
 
 def test_step_can_be_captured_in_a_graph():
