@@ -90,6 +90,27 @@ cd_status cd_forward(int64_t B, int64_t N, int64_t M,
                      void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * cd_forward without a workspace argument, for callers that cannot allocate
+ * device memory (code under graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and checks as cd_forward
+ * (the results are bitwise identical to it); the workspace is a static device
+ * array of CD_FORWARD_NOALLOC_MAX_BYTES bytes inside the library, one per GPU
+ * the library runs on, held until the process ends.  The call allocates
+ * nothing; the first call on a device looks up that device's array address.
+ * Shapes whose cd_workspace_bytes(B, N, M) exceeds the limit (about 8.4
+ * million points in B (N + M)) return CD_ERR_WORKSPACE with the sizes in
+ * cd_last_error(); use cd_forward for them.  Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (two streams, two
+ * threads) race and give undefined results; calls ordered on one stream, or
+ * synchronized, are safe.
+ */
+#define CD_FORWARD_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+cd_status cd_forward_noalloc(int64_t B, int64_t N, int64_t M,
+                             const float *X, const float *Y,
+                             float *dist_xy, int32_t *idx_xy,
+                             float *dist_yx, int32_t *idx_yx, hipStream_t stream);
+
+/*
  * Chamfer reduction (Sec. 2.5): chamfer[b] = w1 * (sum_i dist_xy[b,i]) / N
  * + w2 * (sum_j dist_yx[b,j]) / M.  Sums are accumulated in double in a fixed
  * order and the result rounded once to float32 (bitwise reproducible).

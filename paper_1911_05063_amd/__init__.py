@@ -8,6 +8,7 @@ tensors are not on a ROCm device, the calls raise.
 
 Functions (names follow the C ABI):
   nn_distance(X, Y)                 -> dist_xy, idx_xy, dist_yx, idx_yx
+  nn_distance_noalloc(X, Y, out)    -> the same through cd_forward_noalloc (static workspace)
   chamfer_reduce(dist_xy, dist_yx)  -> chamfer [B]
   f_score(dist_xy, dist_yx, tau)    -> f, precision, recall  [B] each
   metrics(dist_xy, dist_yx, taus)   -> chamfer [B], f / precision / recall [ntau, B]
@@ -30,7 +31,8 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = [
-    "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "chamfer_reduce",
+    "CDError", "LIB_PATH", "library", "workspace_bytes", "nn_distance", "nn_distance_noalloc",
+    "FORWARD_NOALLOC_MAX_BYTES", "chamfer_reduce",
     "f_score", "metrics", "chamfer_backward", "chamfer_backward_pointwise", "chamfer_distance",
     "ChamferDistance", "forward_step", "mesh_sample_faces", "mesh_sample_points",
     "mesh_sample_backward", "MeshSample", "sample_points", "p2s_forward", "p2s_backward",
@@ -105,6 +107,8 @@ def library() -> ctypes.CDLL:
     lib.cd_backward_pointwise.restype = st
     lib.cd_backward_pointwise.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                           ctypes.c_size_t, vp]
+    lib.cd_forward_noalloc.restype = st
+    lib.cd_forward_noalloc.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -206,6 +210,36 @@ def nn_distance(X: torch.Tensor, Y: torch.Tensor, workspace: Optional[torch.Tens
         _check(lib.cd_forward(B, N, M, _ptr(X), _ptr(Y), _ptr(dist_xy), _ptr(idx_xy),
                               _ptr(dist_yx), _ptr(idx_yx), _ptr(workspace), workspace.numel(),
                               ctypes.c_void_p(_stream(dev))), "cd_forward")
+    return dist_xy, idx_xy, dist_yx, idx_yx
+
+
+# The static workspace of cd_forward_noalloc (CD_FORWARD_NOALLOC_MAX_BYTES).
+FORWARD_NOALLOC_MAX_BYTES = 64 << 20
+
+
+def nn_distance_noalloc(X: torch.Tensor, Y: torch.Tensor, out=None
+                        ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """nn_distance through cd_forward_noalloc: the library uses its static
+    per-GPU workspace.  `out` = (dist_xy, idx_xy, dist_yx, idx_yx) preallocated
+    by the caller, else allocated here."""
+    X, Y = _clouds(X, Y)
+    B, N, M = X.shape[0], X.shape[1], Y.shape[1]
+    dev = X.device
+    if out is None:
+        out = (torch.empty((B, N), dtype=torch.float32, device=dev),
+               torch.empty((B, N), dtype=torch.int32, device=dev),
+               torch.empty((B, M), dtype=torch.float32, device=dev),
+               torch.empty((B, M), dtype=torch.int32, device=dev))
+    dist_xy = _expect(out[0], "dist_xy", torch.float32, (B, N), dev)
+    idx_xy = _expect(out[1], "idx_xy", torch.int32, (B, N), dev)
+    dist_yx = _expect(out[2], "dist_yx", torch.float32, (B, M), dev)
+    idx_yx = _expect(out[3], "idx_yx", torch.int32, (B, M), dev)
+    if any(o.data_ptr() != t.data_ptr() for o, t in zip(out, (dist_xy, idx_xy, dist_yx, idx_yx))):
+        raise ValueError("out tensors must be contiguous")
+    with torch.cuda.device(dev):
+        _check(library().cd_forward_noalloc(B, N, M, _ptr(X), _ptr(Y), _ptr(dist_xy),
+                                            _ptr(idx_xy), _ptr(dist_yx), _ptr(idx_yx),
+                                            ctypes.c_void_p(_stream(dev))), "cd_forward_noalloc")
     return dist_xy, idx_xy, dist_yx, idx_yx
 
 

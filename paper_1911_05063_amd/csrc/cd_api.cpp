@@ -109,6 +109,36 @@ cd_status cd_forward(int64_t B, int64_t N, int64_t M, const float *X, const floa
     return CD_OK;
 }
 
+static_assert(CD_FORWARD_NOALLOC_MAX_BYTES == cdk::kForwardScratchBytes,
+              "the header's limit is the scratch array's size");
+
+cd_status cd_forward_noalloc(int64_t B, int64_t N, int64_t M, const float *X, const float *Y,
+                             float *dist_xy, int32_t *idx_xy, float *dist_yx, int32_t *idx_yx,
+                             hipStream_t stream)
+{
+    cd_status s = check_shape(B, N, M);
+    if (s != CD_OK) return s;
+    if (B == 0) return CD_OK;
+    if (!X || !Y || !dist_xy || !idx_xy || !dist_yx || !idx_yx) return invalid("NULL array pointer");
+    const cdk::FwdPlan plan = cdk::plan_forward(B, N, M);
+    const size_t need = cdk::forward_workspace_bytes(plan);
+    if (need > cdk::kForwardScratchBytes) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "cd_forward_noalloc: this shape needs %zu bytes of workspace, more than "
+                      "the %zu of the static scratch array (use cd_forward)",
+                      need, cdk::kForwardScratchBytes);
+        return CD_ERR_WORKSPACE;
+    }
+    if (cdk::forward_tiles(plan) > 2147483647LL) return invalid("too many tiles for one launch");
+    void *ws = nullptr;
+    hipError_t e = cdk::forward_scratch(stream, &ws);
+    if (e != hipSuccess) return hip_failed(e, "cd_forward_noalloc scratch address");
+    const cdk::FwdArgs args{X, Y, dist_xy, idx_xy, dist_yx, idx_yx, ws};
+    e = cdk::launch_forward(plan, args, stream);
+    if (e != hipSuccess) return hip_failed(e, "cd_forward_noalloc launch");
+    return CD_OK;
+}
+
 cd_status cd_reduce(int64_t B, int64_t N, int64_t M, const float *dist_xy, const float *dist_yx,
                     float w1, float w2, float *chamfer, hipStream_t stream)
 {

@@ -41,6 +41,12 @@ int64_t forward_tiles(const FwdPlan &plan);
 
 hipError_t launch_forward(const FwdPlan &plan, const FwdArgs &args, hipStream_t stream);
 
+// The no-allocation forward's workspace: a static device array of this many
+// bytes per GPU.  forward_scratch() gives its address on the device of
+// `stream` (looked up once per device, with that device current).
+constexpr size_t kForwardScratchBytes = size_t(64) << 20;
+hipError_t forward_scratch(hipStream_t stream, void **ptr);
+
 hipError_t launch_reduce(int64_t B, int64_t N, int64_t M, const float *dist_xy,
                          const float *dist_yx, double w1, double w2, float *chamfer,
                          hipStream_t stream);

@@ -42,6 +42,7 @@
 #include "cd_internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace cdk {
 namespace {
@@ -478,6 +479,43 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
 size_t forward_workspace_bytes(const FwdPlan &p) { return ws_offsets(p).total; }
 
 int64_t forward_tiles(const FwdPlan &p) { return p.B * p.nQG * p.nTB; }
+
+// Workspace of cd_forward_noalloc: a file-scope device array, one per GPU the
+// library runs on, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is a stand-in, not a device
+// address): forward_scratch() looks up each device's address once, with that
+// device current, and every use goes through that pointer.
+__device__ __align__(256) unsigned long long scratch[kForwardScratchBytes / 8];
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t forward_scratch(hipStream_t stream, void **ptr)
+{
+    *ptr = nullptr;
+    int dev = 0;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int cur = 0;
+        e = hipGetDevice(&cur);
+        if (e != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        const hipError_t back = cur != dev ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess) return e;
+        if (back != hipSuccess) return back;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream)
 {

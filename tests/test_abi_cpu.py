@@ -76,6 +76,23 @@ def fwd(lib, B, N, M, ptrs=(FAKE,) * 6, ws=FAKE, ws_bytes=1 << 30):
     return lib.cd_forward(B, N, M, *ptrs, ws, ws_bytes, None)
 
 
+def test_noalloc_forward_checks_before_any_launch(lib):
+    # cd_forward_noalloc takes no workspace: its static per-GPU array holds
+    # CD_FORWARD_NOALLOC_MAX_BYTES.  Shapes whose keys need more are refused
+    # before anything is launched (here without a GPU), with the sizes.
+    assert lib.cd_workspace_bytes(1, 2 ** 22, 2 ** 22) == 64 << 20
+    n = 2 ** 22 + 1
+    assert lib.cd_forward_noalloc(1, n, n, *([FAKE] * 6), None) == CD_ERR_WORKSPACE
+    err = lib.cd_last_error()
+    assert b"cd_forward_noalloc" in err and b"67108864" in err
+    assert lib.cd_forward_noalloc(3, 2 ** 21, 2 ** 21, *([FAKE] * 6), None) == CD_ERR_WORKSPACE
+    assert lib.cd_forward_noalloc(1, 0, 5, *([FAKE] * 6), None) == CD_ERR_INVALID_ARG
+    assert lib.cd_forward_noalloc(1, 5, 5, FAKE, None, *([FAKE] * 4), None) == CD_ERR_INVALID_ARG
+    assert lib.cd_forward_noalloc(0, 5, 5, *([FAKE] * 6), None) == CD_OK
+    with open(HEADER) as f:
+        assert "#define CD_FORWARD_NOALLOC_MAX_BYTES ((size_t)64 << 20)" in f.read()
+
+
 def test_forward_rejects_bad_shapes(lib):
     assert fwd(lib, -1, 4, 4) == CD_ERR_INVALID_ARG
     assert fwd(lib, 1, 0, 4) == CD_ERR_INVALID_ARG
