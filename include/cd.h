@@ -29,8 +29,10 @@
  *    point must fit a launch), a negative or NaN tau, or an unaligned
  *    workspace returns CD_ERR_INVALID_ARG.  B == 0 is a no-op that returns
  *    CD_OK.
- *  - Inputs must be finite and their squared distances must not overflow;
- *    other inputs are undefined behaviour.  Outputs must not alias inputs.
+ *  - Inputs must be finite and their squared distances must not overflow
+ *    float32 (coordinates of magnitude at most 2^62, about 4.6e18, always
+ *    satisfy this); other inputs are undefined behaviour (an overflowing
+ *    distance may yield an index of -1).  Outputs must not alias inputs.
  *  - A failed launch returns CD_ERR_HIP; cd_last_error() then holds the HIP
  *    error text for the calling thread.
  */
@@ -295,9 +297,9 @@ cd_status cd_p2s_backward(int64_t B, int64_t S, int64_t nv, int64_t nf, const fl
                           float *gP, float *gV, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Approximate Earth-mover's distance between point clouds (Kaolin Sec. 2.5:
- * "a quadratic approximation of" EMD, by citation of Fan et al., whose EMD is
- * the optimal transport cost with Euclidean ground distance).  Per item: the
+ * Approximate Earth-mover's distance between point clouds (Kaolin Sec. 2.5
+ * names an approximate EMD among its point-cloud metrics, citing Fan et al.,
+ * whose EMD is the optimal transport cost with Euclidean ground distance).  Per item: the
  * transport problem between X [B,N,3] and Y [B,M,3] with uniform masses 1/N,
  * 1/M and cost C_ij = |x_i - y_j|, regularised by entropy and solved with
  * log-domain Sinkhorn iterations (O(N M) work each).  Iteration t of

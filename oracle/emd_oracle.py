@@ -3,8 +3,8 @@
 Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU baseline may
 use it; it shares no code with the HIP library.
 
-Kaolin Sec. 2.5 lists, beside the Chamfer distance, a quadratic approximation of
-the Earth-mover's distance for point clouds, by citation of Fan et al. (2017),
+Kaolin Sec. 2.5 names, beside the Chamfer distance, an approximate form of the
+Earth-mover's distance among its point-cloud metrics, citing Fan et al. (2017),
 whose EMD is the optimal transport cost between the two sets with Euclidean
 ground distance.  Reading taken here: the transport problem with uniform masses
 a_i = 1/N, b_j = 1/M,

@@ -1,5 +1,5 @@
-// Approximate Earth-mover's distance between point clouds (Kaolin Sec. 2.5:
-// a quadratic approximation of EMD, by citation of Fan et al.): the optimal
+// Approximate Earth-mover's distance between point clouds (Kaolin Sec. 2.5
+// names an approximate EMD among its point-cloud metrics, citing Fan et al.): the optimal
 // transport problem with uniform masses a = 1/N, b = 1/M and Euclidean cost
 // C_ij = |x_i - y_j|, regularised by entropy and solved with log-domain
 // Sinkhorn iterations, each touching all N*M pairs.  With a scheduled eps:
