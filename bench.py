@@ -86,6 +86,16 @@ def _sources_sha256(kernel_sources):
     return h.hexdigest()
 
 
+def library_sources_sha256():
+    """sha256 over the library's sources (csrc/, the build script, the C
+    header): names the build a measurement or a profile describes."""
+    import glob
+    srcs = sorted(glob.glob(os.path.join(ROOT, "paper_1911_05063_amd", "csrc", "*")))
+    srcs += [os.path.join(ROOT, "paper_1911_05063_amd", "build.py"),
+             os.path.join(ROOT, "include", "cd.h")]
+    return _sources_sha256([os.path.relpath(p, ROOT) for p in srcs])
+
+
 def ingest_pmc(fetch_dir, write_dir, calib_mib=256):
     """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of cd_forward's kernels, each
     scaled by what the counter reads for the calibration copy of calib_mib MiB."""
@@ -540,6 +550,7 @@ def mesh_step_bench(args):
            "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
+           "library_sha256": library_sources_sha256(),
            "config": {"workload": "mesh_sampling_b16_t200_s16384", "B": B, "triangles": T,
                       "samples": S, "M": M, "taus": [0.005, 0.01, 0.02]},
            "ms_per_call": {"sample_faces+points": samp, "chamfer_fwd_metrics_bwd": cham,
@@ -634,6 +645,7 @@ def p2s_step_bench(args):
            "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
+           "library_sha256": library_sources_sha256(),
            "config": {"workload": w.name, "B": B, "S": S, "nv": nv, "nf": nf},
            "ms_per_call": {"cd_p2s_forward": fwd, "reduce+backward": rest},
            "roofline": {"bound": "alu", "kernel": "cd_p2s_forward (face records + search + merge)",
@@ -731,6 +743,7 @@ def emd_step_bench(args):
            "settle_ms": tm.settle_ms, "settle_steps": tm.settle_steps,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
+           "library_sha256": library_sources_sha256(),
            "config": {"workload": w.name, "B": B, "N": N, "M": M, "iters": EMD_ITERS,
                       "eps": list(EMD_EPS)},
            "ms_per_call": {"cd_emd_forward": fwd, "cd_emd_backward": bwd},
@@ -891,6 +904,7 @@ def chamfer_bench(args):
         "data": "synthetic",
         "config": {"workload": w.name, "kind": w.kind, "B": B, "N": N, "M": M,
                    "taus": list(w.taus), "seed": w.seed},
+        "library_sha256": library_sources_sha256(),
         "ms_per_call": {"forward": statistics.mean(fwd), "forward_median": statistics.median(fwd),
                         "reduce_fscore": statistics.mean(red), "backward": statistics.mean(bwd),
                         "fwd_bwd": ms_per_step, "breakdown_steps": len(red)},
