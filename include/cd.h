@@ -152,9 +152,10 @@ cd_status cd_metrics(int64_t B, int64_t N, int64_t M,
 
 /*
  * Device workspace bytes cd_backward and cd_backward_pointwise need for these
- * sizes (per-block bounds, and per-chunk partial sums when a cloud's senders
- * are split: at most a few hundred MB; 0 for B == 0 or sizes cd_forward
- * rejects).
+ * sizes (0 for B == 0 or sizes cd_forward rejects): per-block bounds, and
+ * per-chunk partial sums when a cloud's senders are split (at most a few
+ * hundred MB), or, where the senders are first sorted by receiver slice, 4
+ * bytes per point of both clouds plus each chunk's slice offsets.
  */
 size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
 
@@ -172,10 +173,12 @@ size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
  * rounded to a 64-bit fixed-point integer (grid 2^-k, with k from a bound on
  * the largest term: per block of up to 2048 receivers (fewer when the clouds
  * are small, so that more workgroups share the work) when the other cloud has at
- * most 16384 points, else per item and cloud; the grid is about 2^-61 times
- * the number of terms times that bound) and the integers are added, so the
- * result is bitwise reproducible run to run; own term + sum are added in
- * double and rounded once.  A point whose index lies
+ * most 16384 points or when the senders are sorted by receiver block first
+ * (large clouds: more than 64 MB of repeated index scans otherwise), else per
+ * item and cloud; the grid is about 2^-61 times the number of terms times
+ * that bound) and the integers are added, so the result is bitwise
+ * reproducible run to run; own term + sum are added in double and rounded
+ * once.  A point whose index lies
  * outside [0, M) / [0, N) contributes nothing (its own and scatter terms are
  * dropped).
  */

@@ -34,6 +34,23 @@
 //    exactly, scaled back, plus the own term (in double), rounded once.
 // Senders are split into chunks only on a side whose scan is much longer than
 // the other's (a few receivers, many senders: one cloud much larger).
+//
+// Bucketed path: every slice workgroup above reads all of its item's sender
+// indices, so index reads grow as (senders) x (slices).  Where those scans
+// would read more than 64 MB (B = 8 clouds of 65536 points: 134 MB; two of
+// 2^20: 4.3 GB), and every side has at most 1024 slices, at most 2^21 senders
+// and on average at most 16384 senders per slice:
+//  * bucket_kernel: per chunk of 2048 senders, counting-sorts them by the
+//    receiver slice of their neighbour (LDS histogram, prefix sum, LDS
+//    cursors) and writes the chunk's entries (sender offset in the chunk,
+//    receiver offset in the slice) grouped by slice, plus the chunk's slice
+//    offsets;
+//  * slice_kernel: per slice, reads each chunk's segment for the slice, so
+//    every sender index is read once in all; the slice holds all of its
+//    terms, so the shift always comes from its own largest term (no bound
+//    pass, no chunk partials) and own + scatter are written directly.
+// The order of entries within a segment depends on the LDS atomics, which
+// does not change the exact sums.
 // A point whose neighbour index lies outside the other cloud contributes
 // nothing (its own term is 0 and it scatters nothing).
 #include <algorithm>
@@ -61,6 +78,17 @@ constexpr int kBoundPer = 1;                // points of each cloud per thread
 constexpr int kBoundBlock = kBoundThreads * kBoundPer;   // points per bound block
 constexpr int kBound = 8;                   // per block: -min xyz, max xyz, max|g_xy|, max|g_yx|
 constexpr int kThreads = 256;
+constexpr int kBucketThreads = 256;         // threads of a bucket workgroup
+constexpr int kBucketPer = 8;               // senders per thread
+constexpr int kChunk = kBucketThreads * kBucketPer;   // senders per bucket chunk
+constexpr int kMaxBucketSlices = 1024;      // slices per item and side (LDS histogram)
+constexpr int kMaxBucketChunks = 1024;      // chunks per item and side (LDS segment table)
+constexpr int64_t kMaxBucketShare = 16384;  // senders per slice on average, at most
+constexpr int64_t kMinBucketScanBytes = int64_t{64} << 20;  // index bytes the slice scans would read
+static_assert(kChunk == 2048 && (kChunk << kSliceBits) <= (int64_t{1} << 32),
+              "bucket entry must fit 32 bits");
+static_assert(kMaxBucketSlices % kBucketThreads == 0 && kMaxBucketChunks == 2 * kBlock,
+              "scan layouts");
 
 struct BwdArgs {
     const float *gxy;   // [B] (per item) or [B, N] (pointwise)
@@ -83,6 +111,13 @@ struct BwdArgs {
     int local[2];       // shift from the workgroup's own terms (one chunk, one pass)
     int64_t chunk[2];   // senders per chunk (a multiple of kPass)
     int64_t poff[2];    // first partial of each side in part
+    // Bucketed path: entries [side][B][nch][kChunk] and per-chunk slice offsets
+    // [side][B][nch][ns + 1].
+    uint32_t *entries;
+    uint32_t *offs;
+    int64_t ebase[2], obase[2];
+    int nch[2];         // bucket chunks of kChunk senders per item
+    int slice_bits;     // log2(slice)
 };
 
 // The clouds as seen from receiving side `side` of item b, with the factors
@@ -431,16 +466,203 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(BwdArgs a, int side)
     write_point(s, p, own, scat);
 }
 
+// One chunk of kChunk senders of one item and side: counting sort by receiver
+// slice.  Senders whose neighbour index lies outside the receiving cloud are
+// dropped.
+__global__ __launch_bounds__(kBucketThreads) void bucket_kernel(BwdArgs a)
+{
+    constexpr int kPerThread = kMaxBucketSlices / kBucketThreads;
+    __shared__ uint32_t hist[kMaxBucketSlices + 1];
+    __shared__ uint32_t wtot[kBucketThreads / kWave];
+    const int tid = threadIdx.x;
+    const int64_t g0 = a.B * a.nch[0];
+    const int side = static_cast<int64_t>(blockIdx.x) < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int nch = a.nch[side], ns = a.ns[side];
+    const int64_t b = g / nch;
+    const int c = static_cast<int>(g % nch);
+    const bool xs = side == 0;
+    const int64_t n_recv = xs ? a.N : a.M, n_send = xs ? a.M : a.N;
+    const int32_t *sidx = (xs ? a.idx_yx : a.idx_xy) + b * n_send;
+    const int64_t q0 = static_cast<int64_t>(c) * kChunk;
+    int32_t iv[kBucketPer];
+#pragma unroll
+    for (int u = 0; u < kBucketPer; ++u) {
+        const int64_t q = q0 + u * kBucketThreads + tid;
+        const int32_t v = q < n_send ? sidx[q] : -1;
+        iv[u] = (v >= 0 && v < n_recv) ? v : -1;
+    }
+    for (int k = tid; k <= ns; k += kBucketThreads) hist[k] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kBucketPer; ++u)
+        if (iv[u] >= 0) atomicAdd(&hist[iv[u] >> a.slice_bits], 1u);
+    __syncthreads();
+    // Exclusive prefix sum over the ns bins (each thread a run of consecutive
+    // bins, then the waves in order); hist[ns] = the chunk's valid senders.
+    const int per = (ns + kBucketThreads - 1) / kBucketThreads;
+    uint32_t loc[kPerThread];
+    uint32_t sum = 0u;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        const int bin = tid * per + k;
+        loc[k] = (k < per && bin < ns) ? hist[bin] : 0u;
+        sum += loc[k];
+    }
+    int total;
+    const int excl = wave_prefix(static_cast<int>(sum), total);
+    if (tid % kWave == 0) wtot[tid / kWave] = static_cast<uint32_t>(total);
+    __syncthreads();
+    uint32_t run = static_cast<uint32_t>(excl), all = 0u;
+#pragma unroll
+    for (int w = 0; w < kBucketThreads / kWave; ++w) {
+        run += w < tid / kWave ? wtot[w] : 0u;
+        all += wtot[w];
+    }
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        const int bin = tid * per + k;
+        if (k < per && bin < ns) {
+            hist[bin] = run;
+            run += loc[k];
+        }
+    }
+    if (tid == 0) hist[ns] = all;
+    __syncthreads();
+    uint32_t *off = a.offs + a.obase[side] + (b * nch + c) * (ns + 1);
+    for (int k = tid; k <= ns; k += kBucketThreads) off[k] = hist[k];
+    __syncthreads();
+    uint32_t *ent = a.entries + a.ebase[side] + (b * nch + c) * static_cast<int64_t>(kChunk);
+#pragma unroll
+    for (int u = 0; u < kBucketPer; ++u) {
+        if (iv[u] >= 0) {
+            const int sl = iv[u] >> a.slice_bits;
+            const uint32_t pos = atomicAdd(&hist[sl], 1u);
+            ent[pos] = (static_cast<uint32_t>(u * kBucketThreads + tid) << kSliceBits) |
+                       static_cast<uint32_t>(iv[u] - (sl << a.slice_bits));
+        }
+    }
+}
+
+// One slice of receivers of one item and side, over the entries every chunk's
+// bucket holds for it.
+template <bool kPointwise>
+__global__ __launch_bounds__(kBlock) void slice_kernel(BwdArgs a)
+{
+    __shared__ unsigned long long acc[3 * kSlice];
+    __shared__ uint32_t pre[kMaxBucketChunks + 1];   // entries before chunk c
+    __shared__ uint32_t seg[kMaxBucketChunks];       // segment start in chunk c
+    __shared__ float red[kBlock / kWave];
+    __shared__ uint32_t wtot[kBlock / kWave];
+    const int tid = threadIdx.x;
+    const int64_t g0 = a.B * a.ns[0];
+    const int side = static_cast<int64_t>(blockIdx.x) < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int ns = a.ns[side], nch = a.nch[side];
+    const int64_t b = g / ns;
+    const int slice = static_cast<int>(g % ns);
+    const Side s = side_of<kPointwise>(a, side, b);
+    const int64_t r0 = static_cast<int64_t>(slice) * a.slice;
+    const int64_t r1 = std::min<int64_t>(r0 + a.slice, s.n_recv);
+
+    // Each thread takes chunks 2 tid and 2 tid + 1: segment starts and lengths.
+    const uint32_t *off = a.offs + a.obase[side] + b * nch * static_cast<int64_t>(ns + 1);
+    uint32_t len[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int c = 2 * tid + k;
+        len[k] = 0u;
+        if (c < nch) {
+            const uint32_t st = off[static_cast<int64_t>(c) * (ns + 1) + slice];
+            seg[c] = st;
+            len[k] = off[static_cast<int64_t>(c) * (ns + 1) + slice + 1] - st;
+        }
+    }
+    float own[kOwn][3];
+#pragma unroll
+    for (int k = 0; k < kOwn; ++k)
+        own_term<kPointwise>(s, std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1), own[k]);
+    for (int t = tid; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
+    int total;
+    const int excl = wave_prefix(static_cast<int>(len[0] + len[1]), total);
+    if (tid % kWave == 0) wtot[tid / kWave] = static_cast<uint32_t>(total);
+    __syncthreads();
+    uint32_t before = static_cast<uint32_t>(excl), all = 0u;
+#pragma unroll
+    for (int w = 0; w < kBlock / kWave; ++w) {
+        before += w < tid / kWave ? wtot[w] : 0u;
+        all += wtot[w];
+    }
+    if (2 * tid < nch) pre[2 * tid] = before;
+    if (2 * tid + 1 < nch) pre[2 * tid + 1] = before + len[0];
+    if (tid == 0) pre[nch] = all;
+    __syncthreads();
+    const int64_t E = all;
+    const uint32_t *ent = a.entries + a.ebase[side] + b * nch * static_cast<int64_t>(kChunk);
+
+    // Flat entry e -> its chunk (the last c with pre[c] <= e) and its term.
+    auto term = [&](int64_t e, float t[3], int &ir) {
+        int lo = 0, hi = nch;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (pre[mid] <= e) lo = mid; else hi = mid;
+        }
+        const uint32_t en = ent[static_cast<int64_t>(lo) * kChunk + seg[lo] + (e - pre[lo])];
+        queued_term<kPointwise>(s, static_cast<int64_t>(lo) * kChunk, r0, en, t, ir);
+    };
+    float hold[kHold][3];
+    int hir[kHold];
+    float m = 0.0f;
+#pragma unroll
+    for (int h = 0; h < kHold; ++h) {
+        const int64_t e = tid + static_cast<int64_t>(h) * kBlock;
+        if (e < E) {
+            term(e, hold[h], hir[h]);
+            m = max_abs3(m, hold[h]);
+        }
+    }
+    for (int64_t e = tid + static_cast<int64_t>(kHold) * kBlock; e < E; e += kBlock) {
+        float t[3];
+        int ir;
+        term(e, t, ir);
+        m = max_abs3(m, t);
+    }
+    const int ks = fixed_shift(group_max<kBlock>(m, red), E);
+#pragma unroll
+    for (int h = 0; h < kHold; ++h)
+        if (tid + static_cast<int64_t>(h) * kBlock < E) add_term(acc, hir[h], hold[h], ks);
+    for (int64_t e = tid + static_cast<int64_t>(kHold) * kBlock; e < E; e += kBlock) {
+        float t[3];
+        int ir;
+        term(e, t, ir);
+        add_term(acc, ir, t, ks);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kOwn; ++k) {
+        const int64_t p = r0 + tid + k * kBlock;
+        if (p < r1) {
+            const unsigned long long *t = acc + 3 * (p - r0);
+            const double scat[3] = {
+                ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
+                ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
+                ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
+            write_point(s, p, own[k], scat);
+        }
+    }
+}
+
 int64_t ceil_div(int64_t x, int64_t y) { return (x + y - 1) / y; }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct BwdPlan {
-    int nblk, slice;
-    int ns[2], nc[2], local[2];
-    bool need_bound;
+    int nblk, slice, slice_bits;
+    int ns[2], nc[2], local[2], nch[2];
+    bool need_bound, bucketed;
     int64_t chunk[2];
     size_t bpart_bytes, shift_bytes, part_elems[2];
+    size_t entry_elems[2], off_elems[2];
 };
 
 BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
@@ -454,12 +676,29 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
     // anyway, and more of them in flight shortens the few dependent memory
     // rounds that bound a small launch (more than one per CU measured slower).
     p.slice = kSlice;
+    p.slice_bits = kSliceBits;
     while (p.slice > kMinSlice &&
-           2 * B * (ceil_div(N, p.slice) + ceil_div(M, p.slice)) <= kCUs)
+           2 * B * (ceil_div(N, p.slice) + ceil_div(M, p.slice)) <= kCUs) {
         p.slice /= 2;
+        --p.slice_bits;
+    }
+    p.bucketed = true;
     for (int s = 0; s < 2; ++s) {
         p.ns[s] = static_cast<int>(ceil_div(n_recv[s], p.slice));
         rounds[s] = ceil_div(n_send[s], kPass);
+        p.nch[s] = static_cast<int>(std::min<int64_t>(ceil_div(n_send[s], kChunk), INT32_MAX));
+        if (p.ns[s] > kMaxBucketSlices || p.nch[s] > kMaxBucketChunks ||
+            ceil_div(n_send[s], p.ns[s]) > kMaxBucketShare)
+            p.bucketed = false;
+    }
+    // Bucketing costs a launch and two dependent memory rounds; it pays where
+    // the slices' repeated index scans read much more than the indices once.
+    const int64_t scan_bytes =
+        4 * B * (static_cast<int64_t>(p.ns[0]) * n_send[0] + static_cast<int64_t>(p.ns[1]) * n_send[1]);
+    if (scan_bytes < kMinBucketScanBytes) p.bucketed = false;
+    for (int s = 0; s < 2; ++s) {
+        p.entry_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * kChunk : 0;
+        p.off_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * (p.ns[s] + 1) : 0;
     }
     // A side whose workgroups would scan many more passes than the other's
     // splits its senders into chunks of about the other's length: the long
@@ -472,7 +711,7 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
         p.local[s] = p.nc[s] == 1 && n_send[s] <= kPass;
         p.part_elems[s] = p.nc[s] > 1 ? static_cast<size_t>(B * p.nc[s] * n_recv[s] * 3) : 0;
     }
-    p.need_bound = !(p.local[0] && p.local[1]);
+    p.need_bound = !p.bucketed && !(p.local[0] && p.local[1]);
     p.bpart_bytes = align256(static_cast<size_t>(B * p.nblk) * kBound * 4);
     p.shift_bytes = align256(static_cast<size_t>(B * 2) * 4);
     return p;
@@ -483,6 +722,9 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
 size_t backward_workspace_bytes(int64_t B, int64_t N, int64_t M)
 {
     const BwdPlan p = plan_backward(B, N, M);
+    if (p.bucketed)
+        return align256((p.entry_elems[0] + p.entry_elems[1]) * 4) +
+               align256((p.off_elems[0] + p.off_elems[1]) * 4);
     return p.bpart_bytes + p.shift_bytes + align256((p.part_elems[0] + p.part_elems[1]) * 8);
 }
 
@@ -521,6 +763,25 @@ hipError_t launch_backward(int64_t B, int64_t N, int64_t M, const float *g_xy,
     }
     a.poff[0] = 0;
     a.poff[1] = static_cast<int64_t>(p.part_elems[0]);
+    a.slice_bits = p.slice_bits;
+    if (p.bucketed) {
+        a.entries = reinterpret_cast<uint32_t *>(base);
+        a.offs = reinterpret_cast<uint32_t *>(
+            base + align256((p.entry_elems[0] + p.entry_elems[1]) * 4));
+        a.ebase[0] = 0;
+        a.ebase[1] = static_cast<int64_t>(p.entry_elems[0]);
+        a.obase[0] = 0;
+        a.obase[1] = static_cast<int64_t>(p.off_elems[0]);
+        for (int s = 0; s < 2; ++s) a.nch[s] = p.nch[s];
+        const uint32_t nb = static_cast<uint32_t>(B * (static_cast<int64_t>(p.nch[0]) + p.nch[1]));
+        const uint32_t nsl = static_cast<uint32_t>(B * (static_cast<int64_t>(p.ns[0]) + p.ns[1]));
+        bucket_kernel<<<nb, kBucketThreads, 0, stream>>>(a);
+        if (pointwise)
+            slice_kernel<true><<<nsl, kBlock, 0, stream>>>(a);
+        else
+            slice_kernel<false><<<nsl, kBlock, 0, stream>>>(a);
+        return hipGetLastError();
+    }
     const uint32_t nbound = static_cast<uint32_t>(B * p.nblk);
     const int64_t groups = B * (static_cast<int64_t>(p.ns[0]) * p.nc[0] +
                                 static_cast<int64_t>(p.ns[1]) * p.nc[1]);

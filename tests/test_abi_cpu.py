@@ -343,6 +343,39 @@ def test_huge_batch_counts_are_rejected_without_overflow(lib):
                                      None) == CD_ERR_INVALID_ARG
 
 
+def test_backward_workspace_follows_its_plan(lib):
+    # Where the slices' repeated index scans would read more than 64 MB, the
+    # backward sorts senders by slice first: its workspace is then the
+    # entries (4 bytes per sender slot, chunks of 2048) and each chunk's
+    # slice offsets, linear in the clouds.  Smaller shapes keep the direct
+    # scan (a few KB of bounds, or chunk partials).
+    import math
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+
+    def slice_of(B, N, M):
+        s = 2048
+        while s > 256 and 2 * B * (math.ceil(N / s) + math.ceil(M / s)) <= 256:
+            s //= 2
+        return s
+
+    for B, N, M in ((8, 65536, 65536), (4, 65536, 65536), (1, 200000, 180000),
+                    (4, 70000, 65536), (1, 2 ** 20, 2 ** 20), (2, 2 ** 21, 2 ** 21)):
+        sl = slice_of(B, N, M)
+        ns = [math.ceil(N / sl), math.ceil(M / sl)]
+        nch = [math.ceil(M / 2048), math.ceil(N / 2048)]
+        assert 4 * B * (ns[0] * M + ns[1] * N) >= 64 << 20
+        want = up(4 * B * 2048 * (nch[0] + nch[1])) + up(4 * B * (nch[0] * (ns[0] + 1) + nch[1] * (ns[1] + 1)))
+        assert lib.cd_backward_workspace_bytes(B, N, M) == want, (B, N, M)
+        assert want <= 5 * B * (N + M) + 4 * B * sum(nc * (n + 1) for nc, n in zip(nch, ns)) + 8192
+    # Below the scan volume, or with a slice share above 16384 senders: not bucketed.
+    for B, N, M in ((16, 16384, 16384), (4, 100000, 10000), (32, 2048, 2048)):
+        sl = slice_of(B, N, M)
+        ns = [math.ceil(N / sl), math.ceil(M / sl)]
+        nch = [math.ceil(M / 2048), math.ceil(N / 2048)]
+        bucketed = up(4 * B * 2048 * (nch[0] + nch[1])) + up(4 * B * (nch[0] * (ns[0] + 1) + nch[1] * (ns[1] + 1)))
+        assert lib.cd_backward_workspace_bytes(B, N, M) != bucketed, (B, N, M)
+
+
 def test_forward_workspace_is_linear_in_the_clouds(lib):
     # The forward keeps one 8-byte key per point of each cloud (tiles fold
     # into them with atomic minima), whatever the planner's tiling: 8 B N and
