@@ -3,12 +3,16 @@
 // match counts.  One kernel serves cd_reduce (Chamfer only), cd_fscore (one
 // threshold) and cd_metrics (Chamfer and up to 4 thresholds per pass), so the
 // three share one accumulation order and agree bitwise.  One 1024-thread
-// workgroup per item: each thread sums its elements in order (in double: the
-// rows are long, and a float32 running sum over 1e5 terms could drift past
-// 1e-5 relative) with 16 loads in flight (32 for the first group: both
-// arrays at once), counts come from wave ballots, and
-// a single reduction (wave shuffles, then the 16 waves in order) combines
-// everything, so the results are bitwise reproducible.
+// workgroup per item.  Each thread sums, in order and in double (the rows are
+// long, and a float32 running sum over 1e5 terms could drift past 1e-5
+// relative), the four consecutive elements of every 16-byte piece it loads
+// (thread t takes pieces t, t + 1024, ...; 8 pieces per array in flight), and counts its
+// matches per threshold in integers.  The waves then combine their lanes with
+// cross-lane moves in a fixed pattern (DPP quad permutations and mirrors
+// within rows of 16, then the row swaps of gfx950), in which every step adds
+// a value and its partner's in both lanes, so all lanes end with the same
+// bits; one wave combines the 16 waves the same way.  The results are
+// bitwise reproducible.
 #include "cd_internal.h"
 
 #include <algorithm>
@@ -18,11 +22,90 @@ namespace {
 
 constexpr int kBlock = 1024;
 constexpr int kWaves = kBlock / kWave;
-constexpr int kGroup = 16;          // loads in flight per thread
+constexpr int kVec = 4;                    // floats per piece
+constexpr int kGroup = 8;                  // pieces in flight per thread
+constexpr int kStride = kBlock * kVec;     // floats per full step of the workgroup
 
 struct Thresholds {
     float thr[kMaxTaus];
 };
+
+// Four consecutive floats at 4-byte alignment (the rows of an item start at
+// any float): one dword-aligned vector load.
+struct F4 {
+    float v[kVec];
+};
+
+// DPP moves within rows of 16 lanes (bound_ctrl: every lane reads a lane).
+constexpr int kQuadXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kHalfMirror = 0x141;
+constexpr int kMirror = 0x140;
+
+template <int kCtrl>
+__device__ __forceinline__ double dpp_d(double v)
+{
+    const int lo = __builtin_amdgcn_mov_dpp(static_cast<int>(__double2loint(v)), kCtrl, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp(static_cast<int>(__double2hiint(v)), kCtrl, 0xF, 0xF, true);
+    return __hiloint2double(hi, lo);
+}
+
+template <int kCtrl>
+__device__ __forceinline__ unsigned dpp_u(unsigned v)
+{
+    return static_cast<unsigned>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), kCtrl, 0xF, 0xF, true));
+}
+
+// v + (the partner's v) across 16-lane rows (even with odd) or 32-lane halves:
+// the swap returns the lane's own value and its partner's, in an order that
+// depends on the lane, and their sum is the same in both lanes.
+__device__ __forceinline__ double swap16_sum(double v)
+{
+    const auto lo = __builtin_amdgcn_permlane16_swap(__double2loint(v), __double2loint(v), false, false);
+    const auto hi = __builtin_amdgcn_permlane16_swap(__double2hiint(v), __double2hiint(v), false, false);
+    return __hiloint2double(hi[0], lo[0]) + __hiloint2double(hi[1], lo[1]);
+}
+
+__device__ __forceinline__ double swap32_sum(double v)
+{
+    const auto lo = __builtin_amdgcn_permlane32_swap(__double2loint(v), __double2loint(v), false, false);
+    const auto hi = __builtin_amdgcn_permlane32_swap(__double2hiint(v), __double2hiint(v), false, false);
+    return __hiloint2double(hi[0], lo[0]) + __hiloint2double(hi[1], lo[1]);
+}
+
+__device__ __forceinline__ unsigned swap16_sum(unsigned v)
+{
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return r[0] + r[1];
+}
+
+__device__ __forceinline__ unsigned swap32_sum(unsigned v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return r[0] + r[1];
+}
+
+// Sum over the wave; every lane returns the same bits.  Each step adds a
+// lane's value and its partner's (a + b in one lane, b + a in the other).
+__device__ __forceinline__ double wave_sum(double v)
+{
+    v += dpp_d<kQuadXor1>(v);
+    v += dpp_d<kQuadXor2>(v);
+    v += dpp_d<kHalfMirror>(v);
+    v += dpp_d<kMirror>(v);
+    v = swap16_sum(v);
+    return swap32_sum(v);
+}
+
+__device__ __forceinline__ unsigned wave_sum(unsigned v)
+{
+    v += dpp_u<kQuadXor1>(v);
+    v += dpp_u<kQuadXor2>(v);
+    v += dpp_u<kHalfMirror>(v);
+    v += dpp_u<kMirror>(v);
+    v = swap16_sum(v);
+    return swap32_sum(v);
+}
 
 // Chamfer sums (if do_chamfer) and the match counts of thresholds
 // first_tau .. first_tau+NT-1 (NT = 0..4).
@@ -34,95 +117,83 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
                                                          float *chamfer, float *f, float *prec,
                                                          float *rec)
 {
+    constexpr int NC = NT > 0 ? NT : 1;
     __shared__ double dred[kWaves][2];
-    __shared__ unsigned long long ured[kWaves][2 * (NT > 0 ? NT : 1)];
+    __shared__ unsigned ured[kWaves][2 * NC];
     const int64_t b = blockIdx.x;
-    const float *a = dxy + b * N;
-    const float *c = dyx + b * M;
-    float thr[NT > 0 ? NT : 1];
+    const int tid = threadIdx.x;
+    float thr[NC];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) thr[t] = th.thr[first_tau + t];
+    for (int t = 0; t < NC; ++t) thr[t] = NT > 0 ? th.thr[first_tau + t] : 0.0f;
     double sx = 0.0, sy = 0.0;
-    unsigned long long cp[NT > 0 ? NT : 1], cr[NT > 0 ? NT : 1];
+    unsigned cp[NC], cr[NC];
 #pragma unroll
-    for (int t = 0; t < (NT > 0 ? NT : 1); ++t) cp[t] = cr[t] = 0ull;
-    // Groups of kGroup full strides (no bounds checks, all loads in flight;
-    // unrolled by hand because loops holding ballots are not unrolled by the
-    // compiler), then the remaining full strides as one guarded group, then
-    // one partial stride.  Every lane runs the same trip counts, so the
-    // ballots see the full wave.
-    auto take = [&](float v, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1]) {
+    for (int t = 0; t < NC; ++t) cp[t] = cr[t] = 0u;
+
+    auto take = [&](float v, double &sum, unsigned (&cnt)[NC]) {
         if (do_chamfer) sum += static_cast<double>(v);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v < thr[t]));
+        for (int t = 0; t < NT; ++t) cnt[t] += v < thr[t] ? 1u : 0u;
     };
-    auto pass = [&](const float *p, int64_t n, double &sum, unsigned long long (&cnt)[NT > 0 ? NT : 1],
-                    int64_t s) {
-        const int64_t full = n / kBlock;
-        for (; s + kGroup <= full; s += kGroup) {
-            float v[kGroup];
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u) v[u] = p[(s + u) * kBlock + threadIdx.x];
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
-                if (do_chamfer) sum += static_cast<double>(v[u]);
-#pragma unroll
-                for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v[u] < thr[t]));
-            }
-        }
-        if (s < full) {
-            // The remaining (fewer than kGroup) full strides, loads in flight
-            // together; the guard is the same for every lane.
-            float v[kGroup];
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u)
-                v[u] = s + u < full ? p[(s + u) * kBlock + threadIdx.x] : 0.0f;
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
-                if (s + u < full) {
-                    if (do_chamfer) sum += static_cast<double>(v[u]);
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(v[u] < thr[t]));
-                }
-            }
-            s = full;
-        }
-        const int64_t i = full * kBlock + threadIdx.x;
-        const bool in = i < n;
-        const float v = in ? p[i] : 0.0f;
-        if (do_chamfer && in) sum += static_cast<double>(v);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) cnt[t] += __popcll(__ballot(in && v < thr[t]));
-    };
-    // The first group of each array is loaded together (one memory round
-    // instead of two when both arrays have a full group); the sums still take
-    // every array's elements in order.
-    int64_t s0 = 0;
-    if (N / kBlock >= kGroup && M / kBlock >= kGroup) {
-        float va[kGroup], vc[kGroup];
+    // Full steps in groups of kGroup pieces (all loads in flight; the last
+    // group guarded, the guard the same for every thread), then the tail of
+    // fewer than kStride floats, one float per thread and round.  The first
+    // group of both arrays is loaded together (one memory round, not two);
+    // each array's elements are still summed in their own order.
+    const float *a = dxy + b * N, *c = dyx + b * M;
+    const F4 *a4 = reinterpret_cast<const F4 *>(a), *c4 = reinterpret_cast<const F4 *>(c);
+    const int64_t fa = N / kStride, fc = M / kStride;
+    {
+        F4 va[kGroup], vc[kGroup];
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
-            va[u] = a[u * kBlock + threadIdx.x];
-            vc[u] = c[u * kBlock + threadIdx.x];
+            if (u < fa) va[u] = a4[u * kBlock + tid];
+            if (u < fc) vc[u] = c4[u * kBlock + tid];
         }
 #pragma unroll
-        for (int u = 0; u < kGroup; ++u) take(va[u], sx, cp);
+        for (int u = 0; u < kGroup; ++u) {
+            if (u < fa) {
 #pragma unroll
-        for (int u = 0; u < kGroup; ++u) take(vc[u], sy, cr);
-        s0 = kGroup;
-    }
-    pass(a, N, sx, cp, s0);
-    pass(c, M, sy, cr, s0);
-    // One reduction for everything: sums over the wave by shuffles (counts are
-    // already per wave: every lane holds the wave's ballot totals), then the
-    // waves in order.
+                for (int i = 0; i < kVec; ++i) take(va[u].v[i], sx, cp);
+            }
+        }
 #pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        sx += __shfl_xor(sx, off, kWave);
-        sy += __shfl_xor(sy, off, kWave);
+        for (int u = 0; u < kGroup; ++u) {
+            if (u < fc) {
+#pragma unroll
+                for (int i = 0; i < kVec; ++i) take(vc[u].v[i], sy, cr);
+            }
+        }
     }
-    const int w = threadIdx.x / kWave;
-    if ((threadIdx.x % kWave) == 0) {
+    auto pass = [&](const float *p, const F4 *p4, int64_t n, int64_t full, double &sum,
+                    unsigned (&cnt)[NC]) {
+        for (int64_t s0 = kGroup; s0 < full; s0 += kGroup) {
+            F4 v[kGroup];
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u)
+                if (s0 + u < full) v[u] = p4[(s0 + u) * kBlock + tid];
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                if (s0 + u < full) {
+#pragma unroll
+                    for (int i = 0; i < kVec; ++i) take(v[u].v[i], sum, cnt);
+                }
+            }
+        }
+        for (int64_t i = full * kStride + tid; i < n; i += kBlock) take(p[i], sum, cnt);
+    };
+    pass(a, a4, N, fa, sx, cp);
+    pass(c, c4, M, fc, sy, cr);
+
+    sx = wave_sum(sx);
+    sy = wave_sum(sy);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        cp[t] = wave_sum(cp[t]);
+        cr[t] = wave_sum(cr[t]);
+    }
+    const int w = tid / kWave, lane = tid % kWave;
+    if (lane == 0) {
         dred[w][0] = sx;
         dred[w][1] = sy;
 #pragma unroll
@@ -132,26 +203,30 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0 && do_chamfer) {
-        double tx = 0.0, ty = 0.0;
-        for (int v = 0; v < kWaves; ++v) {
-            tx += dred[v][0];
-            ty += dred[v][1];
-        }
+    if (w != 0) return;
+    // Wave 0: lane v < kWaves takes wave v's values, the other lanes zeros
+    // (exact), and the wave sums them in the same fixed pattern.  Lane 0 then
+    // writes the Chamfer value and lane 1 + t threshold t's F, P and R: the
+    // lanes run one instruction stream on their own counts.
+    const bool has = lane < kWaves;
+    const double tx = wave_sum(has ? dred[lane][0] : 0.0);
+    const double ty = wave_sum(has ? dred[lane][1] : 0.0);
+    if (lane == 0 && do_chamfer)
         chamfer[b] = static_cast<float>(w1 * (tx / static_cast<double>(N)) +
                                         w2 * (ty / static_cast<double>(M)));
+    unsigned np = 0u, nr = 0u;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const unsigned a_ = wave_sum(has ? ured[lane][2 * t] : 0u);
+        const unsigned c_ = wave_sum(has ? ured[lane][2 * t + 1] : 0u);
+        np = lane == 1 + t ? a_ : np;
+        nr = lane == 1 + t ? c_ : nr;
     }
-    if (threadIdx.x >= 1 && threadIdx.x <= NT) {
-        const int t = threadIdx.x - 1;
-        unsigned long long np = 0, nr = 0;
-        for (int v = 0; v < kWaves; ++v) {
-            np += ured[v][2 * t];
-            nr += ured[v][2 * t + 1];
-        }
+    if (lane >= 1 && lane <= NT) {
         const double P = static_cast<double>(np) / static_cast<double>(N);
         const double R = static_cast<double>(nr) / static_cast<double>(M);
         const double F = (P + R > 0.0) ? (2.0 * P * R) / (P + R) : 0.0;
-        const int64_t o = static_cast<int64_t>(first_tau + t) * B + b;
+        const int64_t o = static_cast<int64_t>(first_tau + lane - 1) * B + b;
         f[o] = static_cast<float>(F);
         if (prec) prec[o] = static_cast<float>(P);
         if (rec) rec[o] = static_cast<float>(R);
