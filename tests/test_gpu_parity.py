@@ -204,6 +204,34 @@ def test_backward_bucketed_senders(B, N, M, kind):
                               g_xy=g_xy, g_yx=g_yx)
 
 
+@pytest.mark.parametrize("B,N,M", [(2, 3000, 2500), (4, 65536, 65536)],
+                         ids=["direct-scan", "bucketed"])
+def test_backward_drops_out_of_range_indices(B, N, M):
+    """A point whose neighbour index lies outside the other cloud contributes
+    nothing (neither its own term nor a scatter term): the same as the oracle
+    fed that point with dL/d dist = 0 and any valid index.  Both backward
+    paths (direct slice scans; senders bucketed by slice)."""
+    print(f"[case] out-of-range indices B={B} N={N} M={M}", flush=True)
+    X, Y = synth.generate("mesh", B, N, M, 81)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    _, ixy, _, iyx = cd.nn_distance(Xg, Yg)
+    ixy_n, iyx_n = gc.to_np(ixy).copy(), gc.to_np(iyx).copy()
+    rng = np.random.default_rng(82)
+    g_xy = rng.normal(0, 1, (B, N)).astype(np.float32)
+    g_yx = rng.normal(0, 1, (B, M)).astype(np.float32)
+    bad_x = rng.random((B, N)) < 0.1
+    bad_y = rng.random((B, M)) < 0.1
+    ixy_n[bad_x] = np.where(rng.random(bad_x.sum()) < 0.5, -1, M + 5)
+    iyx_n[bad_y] = np.where(rng.random(bad_y.sum()) < 0.5, -7, N)
+    gX, gY = cd.chamfer_backward_pointwise(gc.to_gpu(g_xy), gc.to_gpu(g_yx), Xg, Yg,
+                                           gc.to_gpu(ixy_n), gc.to_gpu(iyx_n))
+    # The oracle's equivalent: those points' factor 0, their index any valid one.
+    gx0, gy0 = np.where(bad_x, 0.0, g_xy).astype(np.float32), np.where(bad_y, 0.0, g_yx).astype(np.float32)
+    ix0, iy0 = np.where(bad_x, 0, ixy_n).astype(np.int32), np.where(bad_y, 0, iyx_n).astype(np.int32)
+    gc.assert_grad_exact_sums(gc.to_np(gX), gc.to_np(gY), X, Y, ix0, iy0, g_xy=gx0, g_yx=gy0)
+    assert bool(torch.isfinite(gX).all()) and bool(torch.isfinite(gY).all())
+
+
 def test_autograd_chamfer_distance():
     X, Y = synth.generate("mesh", 3, 700, 900, 31)
     Xg = gc.to_gpu(X).requires_grad_(True)
