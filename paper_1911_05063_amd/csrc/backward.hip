@@ -475,9 +475,14 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(BwdArgs a)
     __shared__ uint32_t hist[kMaxBucketSlices + 1];
     __shared__ uint32_t wtot[kBucketThreads / kWave];
     const int tid = threadIdx.x;
+    // Consecutive chunks of one item and side on one XCD, like the slices that
+    // read their entries (slice_kernel).
+    uint32_t wg = blockIdx.x;
+    const uint32_t xper = gridDim.x / kXcds;
+    if (wg < kXcds * xper) wg = (wg % kXcds) * xper + wg / kXcds;
     const int64_t g0 = a.B * a.nch[0];
-    const int side = static_cast<int64_t>(blockIdx.x) < g0 ? 0 : 1;
-    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int side = static_cast<int64_t>(wg) < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? wg : wg - g0;
     const int nch = a.nch[side], ns = a.ns[side];
     const int64_t b = g / nch;
     const int c = static_cast<int>(g % nch);
@@ -555,9 +560,14 @@ __global__ __launch_bounds__(kBlock) void slice_kernel(BwdArgs a)
     __shared__ float red[kBlock / kWave];
     __shared__ uint32_t wtot[kBlock / kWave];
     const int tid = threadIdx.x;
+    // Workgroups go to the XCDs round-robin: consecutive slices of one item
+    // and side are placed on one XCD, whose L2 then holds that item's clouds.
+    uint32_t wg = blockIdx.x;
+    const uint32_t per = gridDim.x / kXcds;
+    if (wg < kXcds * per) wg = (wg % kXcds) * per + wg / kXcds;
     const int64_t g0 = a.B * a.ns[0];
-    const int side = static_cast<int64_t>(blockIdx.x) < g0 ? 0 : 1;
-    const int64_t g = side == 0 ? blockIdx.x : blockIdx.x - g0;
+    const int side = static_cast<int64_t>(wg) < g0 ? 0 : 1;
+    const int64_t g = side == 0 ? wg : wg - g0;
     const int ns = a.ns[side], nch = a.nch[side];
     const int64_t b = g / ns;
     const int slice = static_cast<int>(g % ns);
