@@ -174,8 +174,8 @@ size_t cd_backward_workspace_bytes(int64_t B, int64_t N, int64_t M);
  * the largest term: per block of up to 2048 receivers (fewer when the clouds
  * are small, so that more workgroups share the work) when the other cloud has at
  * most 16384 points or when the senders are sorted by receiver block first
- * (large clouds: more than 64 MB of repeated index scans otherwise), else per
- * item and cloud; the grid is about 2^-61 times the number of terms times
+ * (where a cloud's senders exceed 16384 points, or where repeated index scans
+ * would read more than 64 MB otherwise), else per item and cloud; the grid is about 2^-61 times the number of terms times
  * that bound) and the integers are added, so the result is bitwise
  * reproducible run to run; own term + sum are added in double and rounded
  * once.  A point whose index lies

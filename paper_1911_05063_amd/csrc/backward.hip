@@ -36,10 +36,12 @@
 // the other's (a few receivers, many senders: one cloud much larger).
 //
 // Bucketed path: every slice workgroup above reads all of its item's sender
-// indices, so index reads grow as (senders) x (slices).  Where those scans
-// would read more than 64 MB (B = 8 clouds of 65536 points: 134 MB; two of
-// 2^20: 4.3 GB), and every side has at most 1024 slices, at most 2^21 senders
-// and on average at most 16384 senders per slice:
+// indices, so index reads grow as (senders) x (slices), and senders beyond one
+// pass need the bound pass and chunk partials.  Where a side's senders exceed
+// one pass, or the scans would read more than 64 MB (B = 8 clouds of 65536
+// points: 134 MB; two of 2^20: 4.3 GB), and every side has at most 1024
+// slices, at most 2^21 senders and on average at most 16384 senders per
+// slice:
 //  * bucket_kernel: per chunk of 2048 senders, counting-sorts them by the
 //    receiver slice of their neighbour (LDS histogram, prefix sum, LDS
 //    cursors) and writes the chunk's entries (sender offset in the chunk,
@@ -692,36 +694,40 @@ BwdPlan plan_backward(int64_t B, int64_t N, int64_t M)
         p.slice /= 2;
         --p.slice_bits;
     }
-    p.bucketed = true;
+    bool feasible = true;
     for (int s = 0; s < 2; ++s) {
         p.ns[s] = static_cast<int>(ceil_div(n_recv[s], p.slice));
         rounds[s] = ceil_div(n_send[s], kPass);
         p.nch[s] = static_cast<int>(std::min<int64_t>(ceil_div(n_send[s], kChunk), INT32_MAX));
         if (p.ns[s] > kMaxBucketSlices || p.nch[s] > kMaxBucketChunks ||
             ceil_div(n_send[s], p.ns[s]) > kMaxBucketShare)
-            p.bucketed = false;
+            feasible = false;
     }
-    // Bucketing costs a launch and two dependent memory rounds; it pays where
-    // the slices' repeated index scans read much more than the indices once.
-    const int64_t scan_bytes =
-        4 * B * (static_cast<int64_t>(p.ns[0]) * n_send[0] + static_cast<int64_t>(p.ns[1]) * n_send[1]);
-    if (scan_bytes < kMinBucketScanBytes) p.bucketed = false;
-    for (int s = 0; s < 2; ++s) {
-        p.entry_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * kChunk : 0;
-        p.off_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * (p.ns[s] + 1) : 0;
-    }
-    // A side whose workgroups would scan many more passes than the other's
-    // splits its senders into chunks of about the other's length: the long
-    // scan is what bounds the kernel's time otherwise.
+    // The direct scan: a side whose workgroups would scan many more passes
+    // than the other's splits its senders into chunks of about the other's
+    // length (the long scan is what bounds the kernel's time otherwise).
     const int64_t target = std::min(rounds[0], rounds[1]);
     for (int s = 0; s < 2; ++s) {
         const int64_t want = ceil_div(rounds[s], target);
         p.chunk[s] = ceil_div(rounds[s], want) * kPass;
         p.nc[s] = static_cast<int>(ceil_div(n_send[s], p.chunk[s]));
         p.local[s] = p.nc[s] == 1 && n_send[s] <= kPass;
-        p.part_elems[s] = p.nc[s] > 1 ? static_cast<size_t>(B * p.nc[s] * n_recv[s] * 3) : 0;
     }
-    p.need_bound = !p.bucketed && !(p.local[0] && p.local[1]);
+    // Bucketing costs a launch and two dependent memory rounds.  It pays where
+    // the direct scan would need the bound pass (a side's senders exceed one
+    // pass) and where its repeated index scans would read much more than the
+    // indices once.
+    const int64_t scan_bytes =
+        4 * B * (static_cast<int64_t>(p.ns[0]) * n_send[0] + static_cast<int64_t>(p.ns[1]) * n_send[1]);
+    const bool direct_local = p.local[0] && p.local[1];
+    p.bucketed = feasible && (!direct_local || scan_bytes >= kMinBucketScanBytes);
+    for (int s = 0; s < 2; ++s) {
+        p.entry_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * kChunk : 0;
+        p.off_elems[s] = p.bucketed ? static_cast<size_t>(B) * p.nch[s] * (p.ns[s] + 1) : 0;
+        p.part_elems[s] = !p.bucketed && p.nc[s] > 1
+                              ? static_cast<size_t>(B * p.nc[s] * n_recv[s] * 3) : 0;
+    }
+    p.need_bound = !p.bucketed && !direct_local;
     p.bpart_bytes = align256(static_cast<size_t>(B * p.nblk) * kBound * 4);
     p.shift_bytes = align256(static_cast<size_t>(B * 2) * 4);
     return p;

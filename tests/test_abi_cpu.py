@@ -343,37 +343,58 @@ def test_huge_batch_counts_are_rejected_without_overflow(lib):
                                      None) == CD_ERR_INVALID_ARG
 
 
-def test_backward_workspace_follows_its_plan(lib):
-    # Where the slices' repeated index scans would read more than 64 MB, the
-    # backward sorts senders by slice first: its workspace is then the
-    # entries (4 bytes per sender slot, chunks of 2048) and each chunk's
-    # slice offsets, linear in the clouds.  Smaller shapes keep the direct
-    # scan (a few KB of bounds, or chunk partials).
+def _backward_plan_bytes(B, N, M):
+    """The backward's workspace for its plan, restated: the direct scan (slices
+    of up to 2048 receivers that scan all senders; per-block bounds, shifts
+    and chunk partials) or, where the direct scan would need the bound pass
+    (senders beyond one pass of 16384) or its repeated index scans would read
+    64 MB or more, senders bucketed by slice (4 bytes per sender slot in
+    chunks of 2048, and each chunk's slice offsets)."""
     import math
     up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    s = 2048
+    while s > 256 and 2 * B * (math.ceil(N / s) + math.ceil(M / s)) <= 256:
+        s //= 2
+    n_recv, n_send = (N, M), (M, N)
+    ns = [math.ceil(r / s) for r in n_recv]
+    nch = [math.ceil(q / 2048) for q in n_send]
+    feasible = all(n <= 1024 and c <= 1024 and math.ceil(q / n) <= 16384
+                   for n, c, q in zip(ns, nch, n_send))
+    rounds = [math.ceil(q / 16384) for q in n_send]
+    target = min(rounds)
+    nc, local = [], []
+    for r, q in zip(rounds, n_send):
+        chunk = math.ceil(r / math.ceil(r / target)) * 16384
+        nc.append(math.ceil(q / chunk))
+        local.append(nc[-1] == 1 and q <= 16384)
+    scan = 4 * B * (ns[0] * n_send[0] + ns[1] * n_send[1])
+    bucketed = feasible and (not all(local) or scan >= 64 << 20)
+    if bucketed:
+        return True, up(4 * B * 2048 * sum(nch)) + up(4 * B * sum(c * (n + 1) for c, n in zip(nch, ns)))
+    nblk = math.ceil(max(N, M) / 1024)
+    parts = sum(B * c * r * 3 for c, r in zip(nc, n_recv) if c > 1)
+    return False, up(B * nblk * 8 * 4) + up(B * 2 * 4) + up(parts * 8)
 
-    def slice_of(B, N, M):
-        s = 2048
-        while s > 256 and 2 * B * (math.ceil(N / s) + math.ceil(M / s)) <= 256:
-            s //= 2
-        return s
 
-    for B, N, M in ((8, 65536, 65536), (4, 65536, 65536), (1, 200000, 180000),
-                    (4, 70000, 65536), (1, 2 ** 20, 2 ** 20), (2, 2 ** 21, 2 ** 21)):
-        sl = slice_of(B, N, M)
-        ns = [math.ceil(N / sl), math.ceil(M / sl)]
-        nch = [math.ceil(M / 2048), math.ceil(N / 2048)]
-        assert 4 * B * (ns[0] * M + ns[1] * N) >= 64 << 20
-        want = up(4 * B * 2048 * (nch[0] + nch[1])) + up(4 * B * (nch[0] * (ns[0] + 1) + nch[1] * (ns[1] + 1)))
-        assert lib.cd_backward_workspace_bytes(B, N, M) == want, (B, N, M)
-        assert want <= 5 * B * (N + M) + 4 * B * sum(nc * (n + 1) for nc, n in zip(nch, ns)) + 8192
-    # Below the scan volume, or with a slice share above 16384 senders: not bucketed.
-    for B, N, M in ((16, 16384, 16384), (4, 100000, 10000), (32, 2048, 2048)):
-        sl = slice_of(B, N, M)
-        ns = [math.ceil(N / sl), math.ceil(M / sl)]
-        nch = [math.ceil(M / 2048), math.ceil(N / 2048)]
-        bucketed = up(4 * B * 2048 * (nch[0] + nch[1])) + up(4 * B * (nch[0] * (ns[0] + 1) + nch[1] * (ns[1] + 1)))
-        assert lib.cd_backward_workspace_bytes(B, N, M) != bucketed, (B, N, M)
+def test_backward_workspace_follows_its_plan(lib):
+    # Bucketed where the direct scan would need the bound pass or would re-read
+    # 64 MB or more of indices (and every slice's share stays small); the
+    # direct scan otherwise.  Either way the workspace is what the plan needs.
+    cases = {(8, 65536, 65536): True, (4, 65536, 65536): True, (1, 200000, 180000): True,
+             (4, 70000, 65536): True, (1, 2 ** 20, 2 ** 20): True, (2, 2 ** 21, 2 ** 21): True,
+             (4, 20000, 30000): True, (16, 16385, 16384): True, (16, 20000, 20000): True,
+             (16, 16384, 16384): False, (4, 100000, 10000): False, (32, 2048, 2048): False,
+             (1, 1024, 1024): False, (1, 300000, 700): False, (2, 5000, 90000): False,
+             (32, 4096, 40000): False}
+    import random
+    rng = random.Random(9)
+    for _ in range(200):
+        cases.setdefault((rng.randint(1, 32), rng.randint(1, 120000), rng.randint(1, 120000)), None)
+    for (B, N, M), want_bucketed in cases.items():
+        bucketed, want = _backward_plan_bytes(B, N, M)
+        if want_bucketed is not None:
+            assert bucketed == want_bucketed, (B, N, M)
+        assert lib.cd_backward_workspace_bytes(B, N, M) == want, (B, N, M, bucketed)
 
 
 def test_forward_workspace_is_linear_in_the_clouds(lib):
