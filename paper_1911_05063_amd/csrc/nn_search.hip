@@ -27,8 +27,7 @@
 //    resident workgroups.  In a launch of one to eight rounds, the last
 //    targets of every group go to small blocks (128) at the end of the grid,
 //    so that the final round is filled with short tiles.  A problem too small
-//    for one round gets blocks of 32..512 targets, about half a round of
-//    tiles.
+//    for one round gets blocks of 32..512 targets, about one round of tiles.
 //  * Each tile folds its packed (distance, batch start) key per x-point and
 //    (distance, lane) key per y-point into one key per point in the workspace
 //    with a 64-bit global atomicMin (the arrays are filled with ~0 first), so
@@ -58,7 +57,7 @@ constexpr int64_t kTargetTiles = 4096;  // workgroups to aim for (4 rounds of 4 
 constexpr int64_t kSlots = 256 * 4;     // workgroups resident at once: 256 CUs x 4
 constexpr int kSmallTB = 128;           // targets per block of the final, small tiles
 constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of 1 to 8 rounds
-constexpr int64_t kSmallLaunchTiles = 512;  // tiles to aim for below one round
+constexpr int64_t kSmallLaunchTiles = 1024;  // tiles to aim for below one round
 constexpr int kMergeThreads = 256;
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
@@ -443,9 +442,9 @@ FwdPlan plan_forward(int64_t B, int64_t N, int64_t M)
     int64_t blocks = ceil_div(M, TB);
     if (groups * blocks < kSlots) {
         // Not one round even with kMinTB: smaller blocks (down to one batch)
-        // until there are about half a round of tiles (two waves per SIMD).
-        // More and smaller tiles measured slower: per-tile set-up and partial
-        // keys grow faster than the parallelism helps.
+        // until there are about one round of tiles (four waves per SIMD).
+        // More and smaller tiles measured slower: per-tile set-up and key
+        // updates grow faster than the parallelism helps.
         const int64_t ts = std::max<int64_t>(
             kBatch,
             ceil_div(ceil_div(M, ceil_div(kSmallLaunchTiles, groups)), kBatch) * kBatch);
