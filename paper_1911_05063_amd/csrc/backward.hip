@@ -24,12 +24,14 @@
 //  * scatter_kernel: a workgroup owns a slice of up to 2048 receivers (256..2048:
 //    small problems take smaller slices, more workgroups) of one cloud and
 //    item and a chunk of the other cloud's senders.  Per pass of 16384
-//    senders it loads their neighbour indices (32 per thread, all in flight
-//    at once), queues the senders that land in its slice in LDS (a wave
-//    prefix sum and one LDS atomic per wave), and then evaluates only the
-//    queued terms, adding them to LDS int64 accumulators (ds_add_u64).  With
-//    one chunk per item it then writes own + scatter directly (the own terms
-//    are loaded at the start); otherwise the slice goes to the workspace.
+//    senders it loads their neighbour indices (32 per thread in 16-byte
+//    loads, all in flight at once), queues the senders that land in its
+//    slice in LDS (a wave prefix sum from ballots and one LDS atomic per
+//    wave), and then evaluates only the queued terms, adding them to LDS int64
+//    accumulators (ds_add_u64).  With one chunk per item it then writes own +
+//    scatter directly (the own terms' loads go out with the first ones, and
+//    nothing waits on them before the output); otherwise the slice goes to
+//    the workspace.
 //  * finalize_kernel: per receiver, the chunks' integer partials summed
 //    exactly, scaled back, plus the own term (in double), rounded once.
 // Senders are split into chunks only on a side whose scan is much longer than
@@ -91,6 +93,11 @@ static_assert(kChunk == 2048 && (kChunk << kSliceBits) <= (int64_t{1} << 32),
               "bucket entry must fit 32 bits");
 static_assert(kMaxBucketSlices % kBucketThreads == 0 && kMaxBucketChunks == 2 * kBlock,
               "scan layouts");
+
+// Four consecutive int32 (a 16-byte load on dword alignment).
+struct I4 {
+    int32_t x, y, z, w;
+};
 
 struct BwdArgs {
     const float *gxy;   // [B] (per item) or [B, N] (pointwise)
@@ -241,6 +248,65 @@ __device__ __forceinline__ void own_term(const Side &s, int64_t p, float own[3])
     for (int c = 0; c < 3; ++c) own[c] = g2 * (s.R[3 * p + c] - s.S[3 * qn + c]);
 }
 
+// The own terms of a thread's kOwn receivers (r0 + tid + k kBlock, clamped
+// into the slice), loaded in two steps so that nothing waits on them before
+// the output: the receivers' coordinates and neighbour indices with the
+// kernel's first loads, the neighbours' coordinates once those have arrived.
+// The receivers' coordinates go to the slice's copy in LDS (`rs`, 3 floats
+// per receiver from r0), which the queued terms read too.  The arithmetic is
+// own_term's.
+template <bool kPointwise>
+struct OwnTerms {
+    int32_t nb[kOwn];
+    float r[kOwn][3], q[kOwn][3], g[kOwn];
+    int o[kOwn];   // receiver offset in the slice
+
+    __device__ __forceinline__ void fetch(const Side &s, int64_t r0, int64_t r1, int tid)
+    {
+#pragma unroll
+        for (int k = 0; k < kOwn; ++k) {
+            const int64_t p = std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1);
+            o[k] = static_cast<int>(p - r0);
+            nb[k] = s.ridx[p];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) r[k][c] = s.R[3 * p + c];
+            g[k] = kPointwise ? s.gr[p] : 0.0f;
+        }
+    }
+    // Several threads may write the slice's last receiver: the same values.
+    __device__ __forceinline__ void stage(float *rs) const
+    {
+#pragma unroll
+        for (int k = 0; k < kOwn; ++k)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) rs[3 * o[k] + c] = r[k][c];
+    }
+    __device__ __forceinline__ bool valid(const Side &s, int k) const
+    {
+        return nb[k] >= 0 && nb[k] < s.n_send;
+    }
+    __device__ __forceinline__ void fetch_neighbours(const Side &s)
+    {
+#pragma unroll
+        for (int k = 0; k < kOwn; ++k) {
+            const int64_t qn = valid(s, k) ? nb[k] : 0;
+#pragma unroll
+            for (int c = 0; c < 3; ++c) q[k][c] = s.S[3 * qn + c];
+        }
+    }
+    __device__ __forceinline__ float g2(const Side &s, int k) const
+    {
+        return valid(s, k) ? (kPointwise ? 2.0f * g[k] : s.g2r) : 0.0f;
+    }
+    // With the receivers' coordinates from the staged copy rs.
+    __device__ __forceinline__ void term(const Side &s, const float *rs, int k, float own[3]) const
+    {
+        const float gk = g2(s, k);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) own[c] = gk * (rs[3 * o[k] + c] - q[k][c]);
+    }
+};
+
 // Own term plus the scatter sum (double), rounded once.
 __device__ __forceinline__ void write_point(const Side &s, int64_t p, const float own[3],
                                             const double scat[3])
@@ -252,17 +318,16 @@ __device__ __forceinline__ void write_point(const Side &s, int64_t p, const floa
 
 // Term -2 g(s) (s - r) of queue entry e (sender offset from `base` in the
 // high bits, receiver offset from r0 in the low kSliceBits); ir = receiver
-// offset.
+// offset; the receiver's coordinates from the slice's copy rs in LDS.
 template <bool kPointwise>
-__device__ __forceinline__ void queued_term(const Side &s, int64_t base, int64_t r0, uint32_t e,
-                                            float t[3], int &ir)
+__device__ __forceinline__ void queued_term(const Side &s, int64_t base, const float *rs,
+                                            uint32_t e, float t[3], int &ir)
 {
     const int64_t q = base + (e >> kSliceBits);
     ir = static_cast<int>(e & (kSlice - 1));
-    const int64_t i = r0 + ir;
     const float g2 = g2_send<kPointwise>(s, q);
 #pragma unroll
-    for (int d = 0; d < 3; ++d) t[d] = -(g2 * (s.S[3 * q + d] - s.R[3 * i + d]));
+    for (int d = 0; d < 3; ++d) t[d] = -(g2 * (s.S[3 * q + d] - rs[3 * ir + d]));
 }
 
 __device__ __forceinline__ void add_term(unsigned long long *acc, int ir, const float t[3], int ks)
@@ -275,6 +340,74 @@ __device__ __forceinline__ void add_term(unsigned long long *acc, int ir, const 
 __device__ __forceinline__ float max_abs3(float m, const float t[3])
 {
     return fmaxf(m, fmaxf(fabsf(t[0]), fmaxf(fabsf(t[1]), fabsf(t[2]))));
+}
+
+// The terms of queue entries e0 + tid + h kBlock, h < H, with all their loads
+// in flight together: an entry at or past n (n > e0) repeats entry n - 1, so
+// every load is of a queued sender and no branch splits the loads.  Returns the
+// largest component of the entries before n.
+template <int H, bool kPointwise>
+__device__ __forceinline__ float hold_terms(const Side &s, int64_t base, const float *rs,
+                                            const uint32_t *queue, int e0, int n, int tid,
+                                            float hold[][3], int hir[])
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        const int e = e0 + tid + h * kBlock;
+        queued_term<kPointwise>(s, base, rs, queue[min(e, n - 1)], hold[h], hir[h]);
+    }
+#pragma unroll
+    for (int h = 0; h < H; ++h)
+        if (e0 + tid + h * kBlock < n) m = max_abs3(m, hold[h]);
+    return m;
+}
+
+// The neighbour indices of one pass of kBlock * kIdx senders from sp, avail
+// of them left in the chunk: iv[4 u + k] is sender 4 (u kBlock + tid) + k,
+// -1 past the end.  The first NU groups u are loaded four senders at a time
+// (kFull: the whole pass lies in the chunk); a group reaching past the end
+// loads the last four senders instead and picks its own; groups from NU on
+// lie past the end.  NU = 0: fewer than four senders, loaded one by one.
+template <int NU, bool kFull>
+__device__ __forceinline__ void load_pass(const int32_t *sp, int avail, int tid,
+                                          int32_t iv[kIdx])
+{
+    if (NU == 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int o = 4 * tid + k;
+            const int32_t e = sp[min(o, avail - 1)];
+            iv[k] = o < avail ? e : -1;
+        }
+    } else if (kFull) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const I4 v = *reinterpret_cast<const I4 *>(sp + 4 * (u * kBlock + tid));
+            iv[4 * u] = v.x;
+            iv[4 * u + 1] = v.y;
+            iv[4 * u + 2] = v.z;
+            iv[4 * u + 3] = v.w;
+        }
+    } else {
+        I4 v[NU > 0 ? NU : 1];
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+            v[u] = *reinterpret_cast<const I4 *>(sp + min(4 * (u * kBlock + tid), avail - 4));
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int o = 4 * (u * kBlock + tid);
+            const int d = o - min(o, avail - 4);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int i = k + d;
+                const int32_t e = i == 0 ? v[u].x : i == 1 ? v[u].y : i == 2 ? v[u].z : v[u].w;
+                iv[4 * u + k] = o + k < avail ? e : -1;
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 4 * (NU == 0 ? 1 : NU); j < kIdx; ++j) iv[j] = -1;
 }
 
 // Exclusive prefix sum of v over the wave (lane order) and the wave's total.
@@ -296,6 +429,7 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
 {
     __shared__ unsigned long long acc[3 * kSlice];
     __shared__ uint32_t queue[kPass];
+    __shared__ float rs[3 * kSlice];
     __shared__ float red[kBlock / kWave];
     __shared__ uint32_t qcount;
     const int tid = threadIdx.x;
@@ -320,14 +454,11 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
     const int64_t r1 = std::min<int64_t>(r0 + a.slice, s.n_recv);
     const bool local = a.local[side] != 0;
 
-    // Own terms of this thread's receivers (with one chunk; otherwise the
-    // finalize pass adds them): independent of the scatter, so loaded first.
-    float own[kOwn][3];
-    if (nc == 1) {
-#pragma unroll
-        for (int k = 0; k < kOwn; ++k)
-            own_term<kPointwise>(s, std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1), own[k]);
-    }
+    // Own terms of this thread's receivers (used with one chunk; otherwise
+    // the finalize pass adds them): independent of the scatter, so their
+    // loads are issued first.
+    OwnTerms<kPointwise> own;
+    own.fetch(s, r0, r1, tid);
 
     for (int t = tid; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
     if (tid == 0) qcount = 0u;
@@ -354,72 +485,109 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
 
     const int64_t q0 = c * a.chunk[side];
     const int64_t q1 = std::min<int64_t>(q0 + a.chunk[side], s.n_send);
-    for (int64_t base = q0; base < q1; base += kPass) {
-        // The pass's neighbour indices, all loads in flight together; queue
-        // the senders whose neighbour lies in the slice.
+    const int32_t r0i = static_cast<int32_t>(r0);
+    const uint32_t slen = static_cast<uint32_t>(r1 - r0);
+    // One pass of senders from `base`: their neighbour indices, and the ones
+    // landing in the slice queued in LDS; returns the queue's length.
+    auto queue_pass = [&](int64_t base) -> int {
+        // The pass's neighbour indices, four consecutive senders per 16-byte
+        // load, all loads in flight together.  Which form runs is the same for
+        // the whole workgroup, so no lane's loads wait on another's.
         int32_t iv[kIdx];
+        const int32_t *sp = s.sidx + base;
+        const int avail = static_cast<int>(std::min<int64_t>(q1 - base, kPass));
+        if (avail == kPass)
+            load_pass<kIdx / 4, true>(sp, avail, tid, iv);
+        else if (avail > 4 * kBlock * (kIdx / 8))
+            load_pass<kIdx / 4, false>(sp, avail, tid, iv);
+        else if (avail > 4 * kBlock * (kIdx / 16))
+            load_pass<kIdx / 8, false>(sp, avail, tid, iv);
+        else if (avail > 4 * kBlock)
+            load_pass<kIdx / 16, false>(sp, avail, tid, iv);
+        else if (avail >= 4)
+            load_pass<1, false>(sp, avail, tid, iv);
+        else
+            load_pass<0, false>(sp, avail, tid, iv);
+        // Queue the senders whose neighbour lies in the slice: bit j of `hit`
+        // for iv[j]; the wave's exclusive prefix of the per-lane counts from
+        // one ballot per bit of the count.
+        uint32_t hit = 0u;
 #pragma unroll
-        for (int u = 0; u < kIdx; ++u) {
-            const int64_t q = base + static_cast<int64_t>(u) * kBlock + tid;
-            iv[u] = q < q1 ? s.sidx[q] : -1;
+        for (int j = 0; j < kIdx; ++j)
+            hit |= (static_cast<uint32_t>(iv[j] - r0i) < slen ? 1u : 0u) << j;
+        // The receivers' coordinates and own neighbour indices arrived before
+        // these.  Every pass stages and fetches them (the same values): done
+        // conditionally, the compiler's wait counts would assume the fetch in
+        // flight and wait for it here.
+        own.stage(rs);
+        own.fetch_neighbours(s);
+        const int cnt = __popc(hit);
+        uint32_t excl = 0u, total = 0u;
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {   // cnt <= 32
+            const unsigned long long m = __ballot((cnt >> k) & 1);
+            excl += __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                              __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u))
+                    << k;
+            total += static_cast<uint32_t>(__popcll(m)) << k;
         }
-        int cnt = 0;
-#pragma unroll
-        for (int u = 0; u < kIdx; ++u) cnt += (iv[u] >= r0 && iv[u] < r1) ? 1 : 0;
-        int total;
-        const int excl = wave_prefix(cnt, total);
         uint32_t wbase = 0u;
-        if (tid % kWave == 0 && total > 0) wbase = atomicAdd(&qcount, static_cast<uint32_t>(total));
-        uint32_t pos = static_cast<uint32_t>(__shfl(static_cast<int>(wbase), 0, kWave) + excl);
+        if (tid % kWave == 0 && total > 0u) wbase = atomicAdd(&qcount, total);
+        uint32_t pos = __builtin_amdgcn_readfirstlane(wbase) + excl;
 #pragma unroll
-        for (int u = 0; u < kIdx; ++u) {
-            if (iv[u] >= r0 && iv[u] < r1)
-                queue[pos++] = (static_cast<uint32_t>(u * kBlock + tid) << kSliceBits) |
-                               static_cast<uint32_t>(iv[u] - r0);
+        for (int j = 0; j < kIdx; ++j) {
+            if ((hit >> j) & 1u)
+                queue[pos++] = (static_cast<uint32_t>(4 * ((j / 4) * kBlock + tid) + j % 4)
+                                << kSliceBits) |
+                               static_cast<uint32_t>(iv[j] - r0i);
         }
         __syncthreads();
-        const int qlen = static_cast<int>(qcount);
+        return static_cast<int>(qcount);
+    };
 
-        if (local) {
-            // The only pass: the shift comes from the largest queued term.
-            float hold[kHold][3];
-            int hir[kHold];
-            float m = 0.0f;
-#pragma unroll
-            for (int h = 0; h < kHold; ++h) {
-                const int e = tid + h * kBlock;
-                if (e < qlen) {
-                    queued_term<kPointwise>(s, base, r0, queue[e], hold[h], hir[h]);
-                    m = max_abs3(m, hold[h]);
-                }
-            }
-            for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
-                float t[3];
-                int ir;
-                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
-                m = max_abs3(m, t);
-            }
-            ks = fixed_shift(group_max<kBlock>(m, red), qlen);
-#pragma unroll
-            for (int h = 0; h < kHold; ++h)
-                if (tid + h * kBlock < qlen) add_term(acc, hir[h], hold[h], ks);
-            for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
-                float t[3];
-                int ir;
-                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
-                add_term(acc, ir, t, ks);
-            }
-        } else {
-            for (int e = tid; e < qlen; e += kBlock) {
-                float t[3];
-                int ir;
-                queued_term<kPointwise>(s, base, r0, queue[e], t, ir);
-                add_term(acc, ir, t, ks);
-            }
+    float hold[kHold][3];
+    int hir[kHold];
+    if (local) {
+        // The only pass (no loop, so that the compiler's wait counts carry
+        // nothing over from a previous pass): the shift comes from the
+        // largest queued term.
+        const int64_t base = q0;
+        const int qlen = queue_pass(base);
+        float m = 0.0f;
+        if (qlen > kHold / 2 * kBlock)
+            m = hold_terms<kHold, kPointwise>(s, base, rs, queue, 0, qlen, tid, hold, hir);
+        else if (qlen > 0)
+            m = hold_terms<kHold / 2, kPointwise>(s, base, rs, queue, 0, qlen, tid, hold, hir);
+        for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
+            float t[3];
+            int ir;
+            queued_term<kPointwise>(s, base, rs, queue[e], t, ir);
+            m = max_abs3(m, t);
         }
-        __syncthreads();
-        if (tid == 0) qcount = 0u;
-        __syncthreads();
+        ks = fixed_shift(group_max<kBlock>(m, red), qlen);
+#pragma unroll
+        for (int h = 0; h < kHold; ++h)
+            if (tid + h * kBlock < qlen) add_term(acc, hir[h], hold[h], ks);
+        for (int e = tid + kHold * kBlock; e < qlen; e += kBlock) {
+            float t[3];
+            int ir;
+            queued_term<kPointwise>(s, base, rs, queue[e], t, ir);
+            add_term(acc, ir, t, ks);
+        }
+        __syncthreads();   // all sums complete before the output reads them
+    } else {
+        for (int64_t base = q0; base < q1; base += kPass) {
+            const int qlen = queue_pass(base);
+            for (int e0 = 0; e0 < qlen; e0 += kHold * kBlock) {
+                hold_terms<kHold, kPointwise>(s, base, rs, queue, e0, qlen, tid, hold, hir);
+#pragma unroll
+                for (int h = 0; h < kHold; ++h)
+                    if (e0 + tid + h * kBlock < qlen) add_term(acc, hir[h], hold[h], ks);
+            }
+            __syncthreads();
+            if (tid == 0) qcount = 0u;
+            __syncthreads();
+        }
     }
 
     if (nc == 1) {
@@ -432,7 +600,9 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
                     ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
                     ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
                     ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
-                write_point(s, p, own[k], scat);
+                float ownk[3];
+                own.term(s, rs, k, ownk);
+                write_point(s, p, ownk, scat);
             }
         }
     } else {
@@ -551,6 +721,17 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(BwdArgs a)
     }
 }
 
+// The chunk holding flat entry e: the last c with pre[c] <= e.
+__device__ __forceinline__ int chunk_of(const uint32_t *pre, int nch, int64_t e)
+{
+    int lo = 0, hi = nch;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (pre[mid] <= e) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
 // One slice of receivers of one item and side, over the entries every chunk's
 // bucket holds for it.
 template <bool kPointwise>
@@ -577,28 +758,36 @@ __global__ __launch_bounds__(kBlock) void slice_kernel(BwdArgs a)
     const int64_t r0 = static_cast<int64_t>(slice) * a.slice;
     const int64_t r1 = std::min<int64_t>(r0 + a.slice, s.n_recv);
 
-    // Each thread takes chunks 2 tid and 2 tid + 1: segment starts and lengths.
+    // Own terms first (their loads overlap the segment loads' round).
+    float ownv[kOwn][3];
+#pragma unroll
+    for (int k = 0; k < kOwn; ++k)
+        own_term<kPointwise>(s, std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1), ownv[k]);
+    // Each thread takes chunks 2 tid and 2 tid + 1: segment starts and lengths
+    // (loaded for a clamped chunk, so that no branch splits the loads).
     const uint32_t *off = a.offs + a.obase[side] + b * nch * static_cast<int64_t>(ns + 1);
+    uint32_t st[2], en[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int64_t c = std::min(2 * tid + k, nch - 1);
+        st[k] = off[c * (ns + 1) + slice];
+        en[k] = off[c * (ns + 1) + slice + 1];
+    }
+    for (int t = tid; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
     uint32_t len[2];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int c = 2 * tid + k;
-        len[k] = 0u;
-        if (c < nch) {
-            const uint32_t st = off[static_cast<int64_t>(c) * (ns + 1) + slice];
-            seg[c] = st;
-            len[k] = off[static_cast<int64_t>(c) * (ns + 1) + slice + 1] - st;
-        }
+        len[k] = c < nch ? en[k] - st[k] : 0u;
+        if (c < nch) seg[c] = st[k];
     }
-    float own[kOwn][3];
-#pragma unroll
-    for (int k = 0; k < kOwn; ++k)
-        own_term<kPointwise>(s, std::min<int64_t>(r0 + tid + k * kBlock, r1 - 1), own[k]);
-    for (int t = tid; t < 3 * (r1 - r0); t += kBlock) acc[t] = 0ull;
     int total;
     const int excl = wave_prefix(static_cast<int>(len[0] + len[1]), total);
     if (tid % kWave == 0) wtot[tid / kWave] = static_cast<uint32_t>(total);
     __syncthreads();
+    // The slice's receivers, read from the cloud (an LDS copy as in
+    // scatter_kernel would leave room for one workgroup per CU instead of two).
+    const float *rs = s.R + 3 * r0;
     uint32_t before = static_cast<uint32_t>(excl), all = 0u;
 #pragma unroll
     for (int w = 0; w < kBlock / kWave; ++w) {
@@ -614,13 +803,9 @@ __global__ __launch_bounds__(kBlock) void slice_kernel(BwdArgs a)
 
     // Flat entry e -> its chunk (the last c with pre[c] <= e) and its term.
     auto term = [&](int64_t e, float t[3], int &ir) {
-        int lo = 0, hi = nch;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (pre[mid] <= e) lo = mid; else hi = mid;
-        }
+        const int lo = chunk_of(pre, nch, e);
         const uint32_t en = ent[static_cast<int64_t>(lo) * kChunk + seg[lo] + (e - pre[lo])];
-        queued_term<kPointwise>(s, static_cast<int64_t>(lo) * kChunk, r0, en, t, ir);
+        queued_term<kPointwise>(s, static_cast<int64_t>(lo) * kChunk, rs, en, t, ir);
     };
     float hold[kHold][3];
     int hir[kHold];
@@ -659,7 +844,7 @@ __global__ __launch_bounds__(kBlock) void slice_kernel(BwdArgs a)
                 ldexp(static_cast<double>(static_cast<long long>(t[0])), -ks),
                 ldexp(static_cast<double>(static_cast<long long>(t[1])), -ks),
                 ldexp(static_cast<double>(static_cast<long long>(t[2])), -ks)};
-            write_point(s, p, own[k], scat);
+            write_point(s, p, ownv[k], scat);
         }
     }
 }
