@@ -59,6 +59,7 @@ constexpr int kSmallTB = 128;           // targets per block of the final, small
 constexpr int64_t kSmallRounds = 8;     // small tiles only for launches of 1 to 8 rounds
 constexpr int64_t kSmallLaunchTiles = 1024;  // tiles to aim for below one round
 constexpr int kMergeThreads = 256;
+constexpr int64_t kXcds = 8;        // accelerator complex dies of an MI355X
 
 __device__ __forceinline__ float sq_dist(float qx, float qy, float qz, float tx, float ty,
                                          float tz)
@@ -292,48 +293,63 @@ struct P3 {
     float x, y, z;
 };
 
-// Threads of the merge that finish rows: B*N rounded up to whole waves.
-__host__ __device__ __forceinline__ int64_t merge_row_threads(int64_t nx)
+// Merge blocks: per item, ceil(N / kMergeThreads) blocks of rows and then
+// ceil(M / kMergeThreads) blocks of columns.  Workgroups are dispatched to
+// the 8 XCDs round-robin; when B is a multiple of 8, block i runs block
+// (i / 8) of the items b = i % 8 (mod 8), so that one XCD's L2 holds the
+// clouds of its items the rescans read (2 items of 16384 points per XCD at
+// B = 16); otherwise items follow one another.
+__host__ __device__ __forceinline__ int64_t merge_blocks_per_item(int64_t N, int64_t M)
 {
-    return (nx + kWave - 1) / kWave * kWave;
+    return (N + kMergeThreads - 1) / kMergeThreads + (M + kMergeThreads - 1) / kMergeThreads;
 }
 
-// Rows first (threads [0, merge_row_threads(B*N))), then one thread per
-// column.  A wave of rows reads the keys of its 64 x-points (one per lane),
-// then rescans their candidate batches 8 x-points at a time: 8 lanes
-// per x-point, each lane 4 consecutive targets (48 contiguous bytes), and the
-// lowest matching index over the 8 lanes.  The rescan loads are clamped into
-// the cloud instead of guarded, so that two rounds' loads are in flight
-// together.  The keys are read once: non-temporal loads keep them
-// from evicting the coordinates that the rescans read.
+__host__ __device__ __forceinline__ bool merge_by_xcd(int64_t B) { return B % kXcds == 0; }
+
+// A wave of rows reads the keys of its 64 x-points (one per lane), then
+// rescans their candidate batches 8 x-points at a time: 8 lanes per x-point,
+// each lane 4 consecutive targets (48 contiguous bytes), and the lowest
+// matching index over the 8 lanes.  The rescan loads are clamped into the
+// cloud instead of guarded, so that two rounds' loads are in flight together.
+// A column thread rescans the kQ x-points of its key's lane.  The keys are read
+// once: non-temporal loads keep them from evicting the coordinates that the
+// rescans read.
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
                                                               int32_t *ixy, float *dyx,
                                                               int32_t *iyx)
 {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * kMergeThreads + threadIdx.x;
-    const int64_t nx = a.B * a.N;
-    const int64_t nr = merge_row_threads(nx);
-    if (t >= nr + a.B * a.M) return;
-    if (t < nr) {
-        // t < nr: whole waves, so every lane of this wave takes this branch.
+    const int64_t pb = merge_blocks_per_item(a.N, a.M);
+    const int64_t rb = (a.N + kMergeThreads - 1) / kMergeThreads;
+    int64_t b, kb;   // item, block within the item
+    if (merge_by_xcd(a.B)) {
+        const int64_t j = blockIdx.x / kXcds;
+        b = static_cast<int64_t>(blockIdx.x % kXcds) + kXcds * (j / pb);
+        kb = j % pb;
+    } else {
+        b = blockIdx.x / pb;
+        kb = blockIdx.x % pb;
+    }
+    if (b >= a.B) return;
+    if (kb < rb) {
+        // A block of rows of item b: whole waves, every lane of a wave here.
         const int lane = threadIdx.x % kWave;
-        const bool mine = t < nx;
+        const int64_t ibase = kb * kMergeThreads + (threadIdx.x - lane);   // the wave's first row
+        const int64_t i = ibase + lane;
+        const bool mine = i < a.N;
         float val = 0.0f, px = 0.0f, py = 0.0f, pz = 0.0f;
-        int js = a.M, bi = 0;  // candidate batch start (M: none) and item
+        int js = a.M;  // candidate batch start (M: none)
         if (mine) {
-            const int64_t b = t / a.N, i = t - b * a.N;
-            bi = static_cast<int>(b);
             const unsigned long long key = __builtin_nontemporal_load(a.rowkey + b * a.N + i);
             val = __uint_as_float(static_cast<uint32_t>(key >> 32));
             js = static_cast<int>(static_cast<uint32_t>(key));
             js = (js < 0 || js >= a.M) ? a.M : js;  // no key: nothing to rescan
-            const P3 x = reinterpret_cast<const P3 *>(a.X)[t];
+            const P3 x = reinterpret_cast<const P3 *>(a.X)[b * a.N + i];
             px = x.x;
             py = x.y;
             pz = x.z;
         }
-        const int64_t wbase = t - lane;
+        const P3 *Yb = reinterpret_cast<const P3 *>(a.Y + b * a.M * 3);
         const int sub = lane & 7;
         constexpr int kR = 2;  // rescan rounds whose loads are issued together
         for (int r0 = 0; r0 < 8; r0 += kR) {
@@ -345,14 +361,11 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
                 const int src = 8 * (r0 + r) + (lane >> 3);
                 v[r] = __shfl(val, src, kWave);
                 const int j0 = __shfl(js, src, kWave);
-                const int bs = __shfl(bi, src, kWave);
                 qx[r] = __shfl(px, src, kWave);
                 qy[r] = __shfl(py, src, kWave);
                 qz[r] = __shfl(pz, src, kWave);
-                const P3 *Yb =
-                    reinterpret_cast<const P3 *>(a.Y + static_cast<int64_t>(bs) * a.M * 3);
-                // A lane past B*N has j0 = M: every load is target M-1 of item
-                // 0 and no candidate qualifies.
+                // A row past N has j0 = M: every load is target M-1 and no
+                // candidate qualifies.
                 je[r] = j0 + min(kBatch, a.M - j0);
                 const int jl = max(je[r] - 1, 0);
                 jb[r] = j0 + 4 * sub;
@@ -375,16 +388,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
             }
 #pragma unroll
             for (int r = 0; r < kR; ++r) {
-                const int64_t tp = wbase + 8 * (r0 + r) + (lane >> 3);
-                if (sub == 0 && tp < nx) {
-                    dxy[tp] = v[r];
-                    ixy[tp] = cand[r] == 0x7fffffff ? -1 : cand[r];
+                const int64_t ip = ibase + 8 * (r0 + r) + (lane >> 3);
+                if (sub == 0 && ip < a.N) {
+                    dxy[b * a.N + ip] = v[r];
+                    ixy[b * a.N + ip] = cand[r] == 0x7fffffff ? -1 : cand[r];
                 }
             }
         }
     } else {
-        const int64_t u = t - nr;
-        const int64_t b = u / a.M, jy = u - b * a.M;
+        const int64_t jy = (kb - rb) * kMergeThreads + threadIdx.x;
+        if (jy >= a.M) return;
+        const int64_t u = b * a.M + jy;
         const unsigned long long key = __builtin_nontemporal_load(a.colkey + b * a.M + jy);
         const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
         // Candidates: the kQ x-points of the winning lane, as a fixed-length,
@@ -538,8 +552,7 @@ hipError_t launch_forward(const FwdPlan &p, const FwdArgs &f, hipStream_t stream
     key_fill_kernel<<<static_cast<uint32_t>(std::min(ceil_div(nkeys, kFillThreads), kFillBlocks)),
                       kFillThreads, 0, stream>>>(a.rowkey, nkeys);
     search_kernel<<<static_cast<uint32_t>(forward_tiles(p)), kThreads, 0, stream>>>(a);
-    const int64_t total = merge_row_threads(p.B * static_cast<int64_t>(p.N)) + p.B * p.M;
-    merge_kernel<<<static_cast<uint32_t>(ceil_div(total, kMergeThreads)), kMergeThreads, 0,
+    merge_kernel<<<static_cast<uint32_t>(p.B * merge_blocks_per_item(p.N, p.M)), kMergeThreads, 0,
                    stream>>>(a, f.dist_xy, f.idx_xy, f.dist_yx, f.idx_yx);
     return hipGetLastError();
 }
