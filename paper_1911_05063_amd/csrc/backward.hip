@@ -195,26 +195,22 @@ __global__ __launch_bounds__(kBoundThreads) void bound_kernel(BwdArgs a)
         v[6] = fabsf(a.gxy[b] * a.sxy);
         v[7] = fabsf(a.gyx[b] * a.syx);
     }
+    // Loads from clamped indices (a point past a cloud's end repeats its last
+    // point, which the maxima already hold), so that no branch splits them.
 #pragma unroll
     for (int u = 0; u < kBoundPer; ++u) {
         const int64_t j = j0 + u * kBoundThreads;
-        if (j < a.N) {
-            const float *x = a.X + (b * a.N + j) * 3;
+        const int64_t jx = std::min<int64_t>(j, a.N - 1), jy = std::min<int64_t>(j, a.M - 1);
+        const float *x = a.X + (b * a.N + jx) * 3;
+        const float *y = a.Y + (b * a.M + jy) * 3;
 #pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                v[c] = fmaxf(v[c], -x[c]);
-                v[3 + c] = fmaxf(v[3 + c], x[c]);
-            }
-            if (kPointwise) v[6] = fmaxf(v[6], fabsf(a.gxy[b * a.N + j]));
+        for (int c = 0; c < 3; ++c) {
+            v[c] = fmaxf(v[c], fmaxf(-x[c], -y[c]));
+            v[3 + c] = fmaxf(v[3 + c], fmaxf(x[c], y[c]));
         }
-        if (j < a.M) {
-            const float *y = a.Y + (b * a.M + j) * 3;
-#pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                v[c] = fmaxf(v[c], -y[c]);
-                v[3 + c] = fmaxf(v[3 + c], y[c]);
-            }
-            if (kPointwise) v[7] = fmaxf(v[7], fabsf(a.gyx[b * a.M + j]));
+        if (kPointwise) {
+            v[6] = fmaxf(v[6], fabsf(a.gxy[b * a.N + jx]));
+            v[7] = fmaxf(v[7], fabsf(a.gyx[b * a.M + jy]));
         }
     }
 #pragma unroll
@@ -622,6 +618,14 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(BwdArgs a, int side)
     const int64_t b = k / n_recv, p = k - b * n_recv;
     const Side s = side_of<kPointwise>(a, side, b);
     const int nc = a.nc[side];
+    // The own term's receiver and neighbour index go out with the partials'
+    // loads, its neighbour's coordinates once the partials are summed (own_term's
+    // arithmetic).
+    const int32_t nb = s.ridx[p];
+    float r[3];
+#pragma unroll
+    for (int d = 0; d < 3; ++d) r[d] = s.R[3 * p + d];
+    const float gr = kPointwise ? s.gr[p] : 0.0f;
     const long long *src = a.part + a.poff[side] + (b * nc * n_recv + p) * 3;
     unsigned long long sum[3] = {0ull, 0ull, 0ull};
     for (int c = 0; c < nc; ++c) {
@@ -629,12 +633,16 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(BwdArgs a, int side)
         for (int d = 0; d < 3; ++d)
             sum[d] += static_cast<unsigned long long>(src[static_cast<int64_t>(c) * n_recv * 3 + d]);
     }
+    const bool ok = nb >= 0 && nb < s.n_send;
+    const int64_t qn = ok ? nb : 0;
+    const float g2 = ok ? (kPointwise ? 2.0f * gr : s.g2r) : 0.0f;
+    float own[3];
+#pragma unroll
+    for (int d = 0; d < 3; ++d) own[d] = g2 * (r[d] - s.S[3 * qn + d]);
     const int ks = a.shift[b * 2 + side];
     const double scat[3] = {ldexp(static_cast<double>(static_cast<long long>(sum[0])), -ks),
                             ldexp(static_cast<double>(static_cast<long long>(sum[1])), -ks),
                             ldexp(static_cast<double>(static_cast<long long>(sum[2])), -ks)};
-    float own[3];
-    own_term<kPointwise>(s, p, own);
     write_point(s, p, own, scat);
 }
 
