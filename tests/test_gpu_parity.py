@@ -51,6 +51,10 @@ SMALL_CASES = [
     # Large target blocks followed by small ones (and the boundary between
     # them) on a tie-heavy cloud.
     ("grid_dup", 2, 2100, 70000, 13),
+    # B a multiple of 8 (the merge gives each XCD the items b = x mod 8) with
+    # items of several merge blocks and a ragged last one on both sides.
+    ("uniform", 8, 1000, 777, 14),
+    ("grid_dup", 16, 513, 1030, 15),
 ]
 
 
