@@ -433,17 +433,18 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(BwdArgs a)
     // the slices of one item and side read the same sender indices and
     // coordinates, so consecutive groups are placed on one XCD (one L2);
     // chunked shapes keep the plain order, which spreads the heavier side.
-    uint32_t wg = blockIdx.x;
-    if (a.nc[0] == 1 && a.nc[1] == 1) {
-        const uint32_t per = gridDim.x / kXcds;
-        if (wg < kXcds * per) wg = (wg % kXcds) * per + wg / kXcds;
-    }
-    const int64_t g0 = a.B * a.ns[0] * a.nc[0];
+    // (32-bit and branch-free: the launch has fewer than 2^32 workgroups, and
+    // the decode runs before the kernel's first loads.)
+    const uint32_t i = blockIdx.x, per = gridDim.x / kXcds;
+    const bool remap = a.nc[0] == 1 && a.nc[1] == 1 && i < kXcds * per;
+    const uint32_t wg = remap ? (i % kXcds) * per + i / kXcds : i;
+    const uint32_t g0 = static_cast<uint32_t>(a.B) * static_cast<uint32_t>(a.ns[0] * a.nc[0]);
     const int side = wg < g0 ? 0 : 1;
-    const int64_t g = side == 0 ? wg : wg - g0;
+    const uint32_t g = side == 0 ? wg : wg - g0;
     const int ns = a.ns[side], nc = a.nc[side];
-    const int64_t b = g / (static_cast<int64_t>(ns) * nc);
-    const int rest = static_cast<int>(g % (static_cast<int64_t>(ns) * nc));
+    const uint32_t pi = static_cast<uint32_t>(ns * nc);
+    const int64_t b = g / pi;
+    const int rest = static_cast<int>(g % pi);
     const int slice = rest / nc, c = rest % nc;
     const Side s = side_of<kPointwise>(a, side, b);
     const int64_t r0 = static_cast<int64_t>(slice) * a.slice;

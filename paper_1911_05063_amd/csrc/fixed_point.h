@@ -25,14 +25,34 @@ __device__ __forceinline__ long long to_fixed(float x, int k)
     return static_cast<long long>(rintf(ldexpf(x, k)));
 }
 
+// Maximum over the wave, in every lane: DPP moves within rows of 16 lanes
+// (quad permutations, then the half-row and row mirrors), then gfx950's row
+// swaps across rows (register moves only, no LDS round trips).
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f(float v)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kCtrl, 0xF, 0xF, true));
+}
+
+__device__ __forceinline__ float wave_max(float m)
+{
+    m = fmaxf(m, dpp_f<0xB1>(m));    // quad_perm [1,0,3,2]
+    m = fmaxf(m, dpp_f<0x4E>(m));    // quad_perm [2,3,0,1]
+    m = fmaxf(m, dpp_f<0x141>(m));   // row_half_mirror
+    m = fmaxf(m, dpp_f<0x140>(m));   // row_mirror
+    const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    m = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+    const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
 // Maximum of m over the workgroup (kThreadsPerGroup threads, all of which
 // must call it); red holds one float per wave.  Ends with a barrier, so red
 // may be reused afterwards.
 template <int kThreadsPerGroup>
 __device__ __forceinline__ float group_max(float m, float *red)
 {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+    m = wave_max(m);
     if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = m;
     __syncthreads();
     m = red[0];
