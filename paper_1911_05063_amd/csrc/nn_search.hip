@@ -308,12 +308,13 @@ __host__ __device__ __forceinline__ bool merge_by_xcd(int64_t B) { return B % kX
 
 // A wave of rows reads the keys of its 64 x-points (one per lane), then
 // rescans their candidate batches 8 x-points at a time: 8 lanes per x-point,
-// each lane 4 consecutive targets (48 contiguous bytes), and the lowest
-// matching index over the 8 lanes.  The rescan loads are clamped into the
-// cloud instead of guarded, so that two rounds' loads are in flight together.
-// A column thread rescans the kQ x-points of its key's lane.  The keys are read
-// once: non-temporal loads keep them from evicting the coordinates that the
-// rescans read.
+// lane c taking targets c, c + 8, c + 16, c + 24 of the batch (so that one
+// load instruction reads 8 consecutive targets of each of 8 batches), and the
+// lowest matching index over the 8 lanes.  The rescan loads are clamped into
+// the cloud instead of guarded, so that two rounds' loads are in flight
+// together.  Columns likewise, 8 lanes per y-point over the kQ x-points of its
+// key's lane.  The keys are read once: non-temporal loads keep them from
+// evicting the coordinates that the rescans read.
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, float *dxy,
                                                               int32_t *ixy, float *dyx,
@@ -368,9 +369,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
                 // candidate qualifies.
                 je[r] = j0 + min(kBatch, a.M - j0);
                 const int jl = max(je[r] - 1, 0);
-                jb[r] = j0 + 4 * sub;
+                jb[r] = j0 + sub;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) ty[r][q] = Yb[min(jb[r] + q, jl)];
+                for (int q = 0; q < 4; ++q) ty[r][q] = Yb[min(jb[r] + 8 * q, jl)];
             }
             int cand[kR];
 #pragma unroll
@@ -380,7 +381,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
                 for (int q = 3; q >= 0; --q) {
                     const float d =
                         sq_dist(qx[r], qy[r], qz[r], ty[r][q].x, ty[r][q].y, ty[r][q].z);
-                    cand[r] = (jb[r] + q < je[r] && d == v[r]) ? jb[r] + q : cand[r];
+                    cand[r] = (jb[r] + 8 * q < je[r] && d == v[r]) ? jb[r] + 8 * q : cand[r];
                 }
 #pragma unroll
                 for (int off = 1; off < 8; off <<= 1)
@@ -396,28 +397,59 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(KernelArgs a, floa
             }
         }
     } else {
-        const int64_t jy = (kb - rb) * kMergeThreads + threadIdx.x;
-        if (jy >= a.M) return;
-        const int64_t u = b * a.M + jy;
-        const unsigned long long key = __builtin_nontemporal_load(a.colkey + b * a.M + jy);
-        const float val = __uint_as_float(static_cast<uint32_t>(key >> 32));
-        // Candidates: the kQ x-points of the winning lane, as a fixed-length,
-        // fully unrolled scan (indices clamped to the last one) so that all
-        // loads are in flight together.
-        const int64_t i0 = static_cast<int64_t>(static_cast<uint32_t>(key)) * kQ;
-        const int64_t il = min(i0 + kQ, static_cast<int64_t>(a.N)) - 1;
-        const P3 y = reinterpret_cast<const P3 *>(a.Y)[u];
-        const P3 *Xb = reinterpret_cast<const P3 *>(a.X + b * a.N * 3);
-        int64_t found = -1;
-#pragma unroll
-        for (int k = kQ - 1; k >= 0; --k) {
-            const int64_t ii = min(i0 + k, il);
-            const P3 tx = Xb[ii];
-            const float d = sq_dist(tx.x, tx.y, tx.z, y.x, y.y, y.z);
-            found = (d == val) ? ii : found;
+        // A block of columns of item b, rescanned like the rows: a wave takes
+        // its 64 y-points' keys, then 8 y-points at a time with 8 lanes each,
+        // lane c recomputing candidate i0 + c of its y-point, so that one load
+        // instruction reads 8 runs of kQ consecutive x-points (coalesced); the
+        // lowest matching index by a 3-step shuffle minimum.
+        static_assert(kQ == 8, "one candidate x-point per lane of an 8-lane group");
+        const int lane = threadIdx.x % kWave;
+        const int64_t jbase = (kb - rb) * kMergeThreads + (threadIdx.x - lane);   // the wave's first column
+        const int64_t jy = jbase + lane;
+        const bool mine = jy < a.M;
+        float val = 0.0f, yx = 0.0f, yy = 0.0f, yz = 0.0f;
+        int i0 = a.N;   // first candidate (N: none)
+        if (mine) {
+            const unsigned long long key = __builtin_nontemporal_load(a.colkey + b * a.M + jy);
+            val = __uint_as_float(static_cast<uint32_t>(key >> 32));
+            const int64_t c0 = static_cast<int64_t>(static_cast<uint32_t>(key)) * kQ;
+            i0 = c0 < a.N ? static_cast<int>(c0) : a.N;   // no key: nothing to rescan
+            const P3 y = reinterpret_cast<const P3 *>(a.Y)[b * a.M + jy];
+            yx = y.x;
+            yy = y.y;
+            yz = y.z;
         }
-        dyx[u] = val;
-        iyx[u] = static_cast<int32_t>(found);
+        const P3 *Xb = reinterpret_cast<const P3 *>(a.X + b * a.N * 3);
+        const int sub = lane & 7;
+        float v[8], qx[8], qy[8], qz[8];
+        int ic[8], ie[8];
+        P3 tx[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int src = 8 * r + (lane >> 3);
+            v[r] = __shfl(val, src, kWave);
+            const int c0 = __shfl(i0, src, kWave);
+            qx[r] = __shfl(yx, src, kWave);
+            qy[r] = __shfl(yy, src, kWave);
+            qz[r] = __shfl(yz, src, kWave);
+            // A column past M or without a key has c0 = N: the load is
+            // x-point N-1 and no candidate qualifies.
+            ie[r] = c0 + min(kQ, a.N - c0);
+            ic[r] = c0 + sub;
+            tx[r] = Xb[min(ic[r], max(ie[r] - 1, 0))];
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const float d = sq_dist(tx[r].x, tx[r].y, tx[r].z, qx[r], qy[r], qz[r]);
+            int cand = (ic[r] < ie[r] && d == v[r]) ? ic[r] : 0x7fffffff;
+#pragma unroll
+            for (int off = 1; off < 8; off <<= 1) cand = min(cand, __shfl_xor(cand, off, kWave));
+            const int64_t jp = jbase + 8 * r + (lane >> 3);
+            if (sub == 0 && jp < a.M) {
+                dyx[b * a.M + jp] = v[r];
+                iyx[b * a.M + jp] = cand == 0x7fffffff ? -1 : cand;
+            }
+        }
     }
 }
 
