@@ -25,8 +25,8 @@ KINDS = ("uniform", "sphere", "mesh", "gmm", "grid_dup")
 def _cases(seed=2024):
     """24 shapes log-uniform in [1, 40000] (mostly small and ragged), 16 with
     both clouds in [2000, 40000] (several query groups and target blocks,
-    senders beyond one pass), at most 3e8 pairs each, and two launches long
-    enough for the small final target blocks."""
+    senders beyond one pass), at most 3e8 pairs each, two launches long
+    enough for the small final target blocks, and four with B a multiple of 8."""
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < 40:
@@ -41,6 +41,10 @@ def _cases(seed=2024):
             out.append((kind, B, N, M, int(rng.integers(1 << 30))))
     # Launches of one to a few rounds: large target blocks, then small ones.
     out += [("mesh", 4, 8192, 16384, 77), ("gmm", 2, 16385, 30000, 78)]
+    # B a multiple of 8 (the merge gives XCD x the items b = x mod 8), ragged
+    # clouds of several merge blocks, direct and bucketed backward.
+    out += [("uniform", 8, 2500, 777, 79), ("grid_dup", 16, 1300, 3001, 80),
+            ("sphere", 24, 600, 259, 81), ("gmm", 8, 20000, 20001, 82)]
     return out
 
 
