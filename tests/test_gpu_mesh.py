@@ -159,12 +159,14 @@ def test_full_size_mesh_sampling():
     assert np.all(np.abs(gV - rV) <= tol + 1e-30)
 
 
-def test_zero_area_faces_never_chosen_and_reproducible():
-    # 6000 faces (several faces per scan thread), every third one invalid (a
-    # vertex index out of range) and every third one degenerate (a repeated
-    # vertex): no sample may land on either, and the face choice and the
-    # backward are bitwise reproducible.
-    B, n, S = 2, 6000, 50000
+@pytest.mark.parametrize("n", [900, 3000, 6000])
+def test_zero_area_faces_never_chosen_and_reproducible(n):
+    # 900, 3000 and 6000 faces (one face per scan thread, up to four kept in
+    # registers, several stashed between the scan's passes), every third one
+    # invalid (a vertex index out of range) and every third one degenerate (a
+    # repeated vertex): no sample may land on either, and the face choice and
+    # the backward are bitwise reproducible.
+    B, S = 2, 50000
     V, F = synth.triangle_soup(B, n, 81)
     F = F.copy()
     F[:, 0::3, 2] = 3 * n + 5
