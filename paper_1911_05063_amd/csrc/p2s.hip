@@ -250,8 +250,16 @@ __global__ __launch_bounds__(kThreads) void p2s_merge_kernel(int64_t B, int64_t 
     if (k >= B * S) return;
     const int64_t b = k / S, q = k - b * S;
     const uint64_t *p = part + b * nFB * S + q;
+    // Eight blocks' keys in flight at a time (indices past the last block
+    // repeat it: the minimum does not change).
     uint64_t m = ~0ull;
-    for (int i = 0; i < nFB; ++i) m = std::min<uint64_t>(m, p[static_cast<int64_t>(i) * S]);
+    for (int i0 = 0; i0 < nFB; i0 += 8) {
+        uint64_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<int64_t>(min(i0 + u, nFB - 1)) * S];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = std::min<uint64_t>(m, v[u]);
+    }
     dist[k] = __uint_as_float(static_cast<uint32_t>(m >> 32));
     fidx[k] = static_cast<int32_t>(static_cast<uint32_t>(m));
 }
@@ -321,25 +329,40 @@ __global__ __launch_bounds__(kThreads) void p2s_point_grad_kernel(
     const int64_t k = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     if (k >= B * S) return;
     const int64_t b = k / S;
+    // The point, its factor and face, then the face's vertex indices, then the
+    // vertices: three memory rounds with no branch between them (an invalid
+    // face or vertex index reads face / vertex 0 and contributes nothing).
     const int32_t f = fidx[k];
+    float pf[3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) pf[i] = P[3 * k + i];
+    const float gk = g[k];
+    const bool fok = (f >= 0) & (f < nf);
+    const int32_t *t = F + (b * nf + (fok ? f : 0)) * 3;
+    int32_t tv[3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) tv[i] = t[i];
+    const bool ok = fok & face_ok_nb(tv, nv);
+    const float *Vb = V + b * nv * 3;
+    float vf[3][3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int i = 0; i < 3; ++i) vf[j][i] = Vb[3 * static_cast<int64_t>(ok ? tv[j] : 0) + i];
     float gp[3] = {0.0f, 0.0f, 0.0f}, wf[3] = {0.0f, 0.0f, 0.0f};
-    if (f >= 0 && f < nf) {
-        const int32_t *t = F + (b * nf + f) * 3;
-        if (face_ok(t, nv)) {
-            const float *Vb = V + b * nv * 3;
-            double p[3], A[3], Bv[3], C[3], w[3], res[3];
-            for (int i = 0; i < 3; ++i) {
-                p[i] = P[3 * k + i];
-                A[i] = Vb[3 * static_cast<int64_t>(t[0]) + i];
-                Bv[i] = Vb[3 * static_cast<int64_t>(t[1]) + i];
-                C[i] = Vb[3 * static_cast<int64_t>(t[2]) + i];
-            }
-            closest_point(p, A, Bv, C, w, res);
-            const double g2 = 2.0 * static_cast<double>(g[k]);
-            for (int i = 0; i < 3; ++i) {
-                gp[i] = static_cast<float>(g2 * res[i]);
-                wf[i] = static_cast<float>(w[i]);
-            }
+    if (ok) {
+        double p[3], A[3], Bv[3], C[3], w[3], res[3];
+        for (int i = 0; i < 3; ++i) {
+            p[i] = pf[i];
+            A[i] = vf[0][i];
+            Bv[i] = vf[1][i];
+            C[i] = vf[2][i];
+        }
+        closest_point(p, A, Bv, C, w, res);
+        const double g2 = 2.0 * static_cast<double>(gk);
+        for (int i = 0; i < 3; ++i) {
+            gp[i] = static_cast<float>(g2 * res[i]);
+            wf[i] = static_cast<float>(w[i]);
         }
     }
     for (int i = 0; i < 3; ++i) {
