@@ -57,11 +57,14 @@ def _points_close(P_gpu, V, F, fidx, r1, r2):
 
 
 # Cases span one and several sample chunks per item, one and several vertex
-# slices (grid 70: 4900 vertices), ragged last chunks, S = 1 and S = 0.
+# slices (grid 70: 4900 vertices), ragged last chunks, S = 1 and S = 0, and the
+# backward's chunk sizes: 512 samples (most cases), 1024 (grid 10), 2048 (soup
+# 40 x 20) held in registers, and 2560 (520 items: one chunk each) in the loop.
 @pytest.mark.parametrize("maker,B,n,S", [("soup", 3, 200, 5000), ("grid", 2, 40, 7000),
                                          ("soup", 1, 1, 100), ("grid", 4, 3, 1),
                                          ("grid", 1, 70, 40001), ("soup", 2, 1500, 3333),
-                                         ("soup", 2, 5, 0)])
+                                         ("soup", 2, 5, 0), ("grid", 1, 10, 200000),
+                                         ("soup", 40, 20, 12000), ("soup", 520, 10, 2100)])
 def test_sampling_matches_oracle(maker, B, n, S):
     V, F = synth.triangle_soup(B, n, 61) if maker == "soup" else synth.grid_mesh(B, n, 62)
     u, r1, r2 = synth.uniforms(B, S, 63)

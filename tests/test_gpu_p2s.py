@@ -146,7 +146,11 @@ def _check_backward(P, V, F, fidx, g, gP, gV):
     assert np.all(np.abs(gV - rV) <= tolV), np.max(np.abs(gV - rV) - tolV)
 
 
-@pytest.mark.parametrize("B,S,level,seed", [(2, 3001, 2, 41), (1, 40000, 4, 42), (3, 5, 0, 43)])
+# The vertex scatter's chunks: 512 samples (the first three), 1024 (200000
+# points on one item) and 2048 (16 items of 16384, in the full-size test) held
+# in registers, 2560 (520 items: one chunk each) in the loop.
+@pytest.mark.parametrize("B,S,level,seed", [(2, 3001, 2, 41), (1, 40000, 4, 42), (3, 5, 0, 43),
+                                            (1, 200000, 0, 44), (520, 2100, 0, 45)])
 def test_backward_matches_oracle(B, S, level, seed):
     print(f"[case] p2s backward B={B} S={S} level={level}", flush=True)
     P, V, F = synth.p2s_workload(B, S, level, seed)
