@@ -74,20 +74,23 @@ __global__ __launch_bounds__(kThreads) void face_record_kernel(int64_t B, int64_
     const int64_t k = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     if (k >= B * nf) return;
     const int64_t b = k / nf;
-    const int32_t *t = F + 3 * k;
+    // The three vertex indices in one load round, then the three vertices
+    // (vertex 0 in place of an out-of-range index) in the next.
+    const int32_t t[3] = {F[3 * k], F[3 * k + 1], F[3 * k + 2]};
+    const bool ok = face_ok_nb(t, nv);
+    const float *Vb = V + b * nv * 3;
+    double A[3], Bv[3], C[3], e0[3], e1[3], e2[3], n[3];
+    for (int i = 0; i < 3; ++i) {
+        A[i] = Vb[3 * static_cast<int64_t>(ok ? t[0] : 0) + i];
+        Bv[i] = Vb[3 * static_cast<int64_t>(ok ? t[1] : 0) + i];
+        C[i] = Vb[3 * static_cast<int64_t>(ok ? t[2] : 0) + i];
+    }
     float *r = rec + k * kRec;
-    if (!face_ok(t, nv)) {
+    if (!ok) {
         for (int i = 0; i < kRec; ++i) r[i] = 0.0f;
         r[0] = r[1] = r[2] = kFar;
         r[12] = __builtin_inff();
         return;
-    }
-    const float *Vb = V + b * nv * 3;
-    double A[3], Bv[3], C[3], e0[3], e1[3], e2[3], n[3];
-    for (int i = 0; i < 3; ++i) {
-        A[i] = Vb[3 * static_cast<int64_t>(t[0]) + i];
-        Bv[i] = Vb[3 * static_cast<int64_t>(t[1]) + i];
-        C[i] = Vb[3 * static_cast<int64_t>(t[2]) + i];
     }
     for (int i = 0; i < 3; ++i) {
         e0[i] = Bv[i] - A[i];

@@ -108,7 +108,8 @@ __device__ __forceinline__ unsigned wave_sum(unsigned v)
 }
 
 // Chamfer sums (if do_chamfer) and the match counts of thresholds
-// first_tau .. first_tau+NT-1 (NT = 0..4).
+// first_tau .. first_tau+NT-1 (NT = 1..4); F, P and R are written if f is not
+// null.
 template <int NT>
 __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, const float *dxy,
                                                          const float *dyx, double w1, double w2,
@@ -117,14 +118,15 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
                                                          float *chamfer, float *f, float *prec,
                                                          float *rec)
 {
-    constexpr int NC = NT > 0 ? NT : 1;
+    static_assert(NT >= 1 && NT <= 4, "one to four thresholds per pass");
+    constexpr int NC = NT;
     __shared__ double dred[kWaves][2];
     __shared__ unsigned ured[kWaves][2 * NC];
     const int64_t b = blockIdx.x;
     const int tid = threadIdx.x;
     float thr[NC];
 #pragma unroll
-    for (int t = 0; t < NC; ++t) thr[t] = NT > 0 ? th.thr[first_tau + t] : 0.0f;
+    for (int t = 0; t < NC; ++t) thr[t] = th.thr[first_tau + t];
     double sx = 0.0, sy = 0.0;
     unsigned cp[NC], cr[NC];
 #pragma unroll
@@ -137,9 +139,9 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
     };
     // Full steps in groups of kGroup pieces (all loads in flight; the last
     // group guarded, the guard the same for every thread), then the tail of
-    // fewer than kStride floats, one float per thread and round.  The first
-    // group of both arrays is loaded together (one memory round, not two);
-    // each array's elements are still summed in their own order.
+    // fewer than kStride floats, at most kVec per thread.  The first group
+    // and the tails of both arrays are loaded together (one memory round,
+    // not two); each array's elements are still summed in their own order.
     const float *a = dxy + b * N, *c = dyx + b * M;
     const F4 *a4 = reinterpret_cast<const F4 *>(a), *c4 = reinterpret_cast<const F4 *>(c);
     const int64_t fa = N / kStride, fc = M / kStride;
@@ -165,8 +167,7 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
             }
         }
     }
-    auto pass = [&](const float *p, const F4 *p4, int64_t n, int64_t full, double &sum,
-                    unsigned (&cnt)[NC]) {
+    auto pass = [&](const F4 *p4, int64_t full, double &sum, unsigned (&cnt)[NC]) {
         for (int64_t s0 = kGroup; s0 < full; s0 += kGroup) {
             F4 v[kGroup];
 #pragma unroll
@@ -180,10 +181,27 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
                 }
             }
         }
-        for (int64_t i = full * kStride + tid; i < n; i += kBlock) take(p[i], sum, cnt);
     };
-    pass(a, a4, N, fa, sx, cp);
-    pass(c, c4, M, fc, sy, cr);
+    pass(a4, fa, sx, cp);
+    pass(c4, fc, sy, cr);
+    // The tails, fewer than kStride floats per array (at most kVec per
+    // thread): both arrays' loads in one round, at indices clamped into the
+    // array (those past its end are not summed); none if both are empty.
+    if (fa * kStride < N || fc * kStride < M) {
+        const int64_t ia = fa * kStride + tid, ic = fc * kStride + tid;
+        float ta[kVec], tc[kVec];
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+            ta[j] = a[std::min<int64_t>(ia + j * kBlock, N - 1)];
+            tc[j] = c[std::min<int64_t>(ic + j * kBlock, M - 1)];
+        }
+#pragma unroll
+        for (int j = 0; j < kVec; ++j)
+            if (ia + j * kBlock < N) take(ta[j], sx, cp);
+#pragma unroll
+        for (int j = 0; j < kVec; ++j)
+            if (ic + j * kBlock < M) take(tc[j], sy, cr);
+    }
 
     sx = wave_sum(sx);
     sy = wave_sum(sy);
@@ -222,7 +240,7 @@ __global__ __launch_bounds__(kBlock) void metrics_kernel(int64_t N, int64_t M, c
         np = lane == 1 + t ? a_ : np;
         nr = lane == 1 + t ? c_ : nr;
     }
-    if (lane >= 1 && lane <= NT) {
+    if (f && lane >= 1 && lane <= NT) {
         const double P = static_cast<double>(np) / static_cast<double>(N);
         const double R = static_cast<double>(nr) / static_cast<double>(M);
         const double F = (P + R > 0.0) ? (2.0 * P * R) / (P + R) : 0.0;
@@ -271,8 +289,14 @@ hipError_t launch_reduce(int64_t B, int64_t N, int64_t M, const float *dist_xy,
                          const float *dist_yx, double w1, double w2, float *chamfer,
                          hipStream_t stream)
 {
+    // The one-threshold form with its F-score outputs off (its counts cost
+    // nothing measurable here): compiled for the Chamfer sum alone, the kernel
+    // converted each loaded element to double next to its load, spilling and
+    // waiting for every load before issuing the next (6.1 against 4.5 us on
+    // 16 items of 16384 points).  Same sums, same order: bitwise equal to
+    // cd_metrics' Chamfer values.
     Thresholds th{};
-    metrics_kernel<0><<<static_cast<uint32_t>(B), kBlock, 0, stream>>>(
+    metrics_kernel<1><<<static_cast<uint32_t>(B), kBlock, 0, stream>>>(
         N, M, dist_xy, dist_yx, w1, w2, th, 0, 1, B, chamfer, nullptr, nullptr, nullptr);
     return hipGetLastError();
 }
