@@ -821,11 +821,25 @@ def measure_chamfer(step, steps, warmup, settle_ms, breakdown_steps):
             "bwd": [e[2].elapsed_time(e[3]) for e in bd.events]}
 
 
-def config_figures(w, m, rec):
+def max_in_degree(step):
+    """The backward's scatter contention after a step: over all items, the
+    largest number of senders whose nearest neighbour is one receiver (Y
+    points onto an x, X points onto a y), from the step's index outputs
+    (copied to the host after the timed region)."""
+    import numpy as np
+    step.torch.cuda.synchronize()
+    ixy, iyx = step.ixy.cpu().numpy(), step.iyx.cpu().numpy()
+    onto_x = max(int(np.bincount(r, minlength=step.N).max()) for r in iyx)
+    onto_y = max(int(np.bincount(r, minlength=step.M).max()) for r in ixy)
+    return {"onto_x": onto_x, "onto_y": onto_y}
+
+
+def config_figures(w, m, rec, step):
     """Per-workload figures of one measure_chamfer() result."""
     fwd = statistics.mean(m["fwd"])
     credited, executed, issue = forward_fractions(w.B, w.N, w.M, fwd, rec, w.name)
     return {"B": w.B, "N": w.N, "M": w.M, "steps": len(m["timing"].events),
+            "max_in_degree": max_in_degree(step),
             "ms_per_step": m["ms_per_step"],
             "pair_evals_per_s": 2.0 * w.B * w.N * w.M / (m["ms_per_step"] * 1e-3),
             "ms_per_call": {"forward": fwd, "metrics": statistics.mean(m["red"]),
@@ -851,7 +865,7 @@ def per_config(args, main_k, main_fig, rec):
         n = int(min(200, max(10, 50.0 / (probe_ms / probe_n))))
         print(f"[bench] per-config {w.name}: {n} steps", file=sys.stderr, flush=True)
         m = measure_chamfer(step, n, 5, 20.0, min(n, 50))
-        out[w.name] = config_figures(w, m, rec)
+        out[w.name] = config_figures(w, m, rec, step)
         del step
         torch.cuda.empty_cache()
     return out
@@ -886,7 +900,7 @@ def chamfer_bench(args):
     fwd_avg_s = statistics.mean(fwd) * 1e-3
     achieved = FLOPS_PER_PAIR * pairs / fwd_avg_s / 1e12
     rec = valu_record()
-    main_fig = config_figures(w, m, rec)
+    main_fig = config_figures(w, m, rec, step)
     out = {
         "metric": METRIC,
         "value": value,

@@ -54,3 +54,6 @@ def test_bench_prints_one_json_line(args):
             assert all(v > 0 for v in c["ms_per_call"].values()), name
             assert 0 < c["executed_frac"] < 1.0, name
             assert c["valu_issue_frac"] is None or 0 < c["valu_issue_frac"] < 1.0, name
+            # Every receiver count is at least 1 somewhere and at most the senders.
+            deg = c["max_in_degree"]
+            assert 1 <= deg["onto_x"] <= c["M"] and 1 <= deg["onto_y"] <= c["N"], (name, deg)
