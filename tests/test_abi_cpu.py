@@ -181,6 +181,14 @@ def test_mesh_entry_points_reject_bad_args(lib):
             w = lib.cd_mesh_workspace_bytes(B, nv, 10, (2 ** 31 - 1) // B)
             assert 0 < w <= (48 << 20) + 256 and w % 256 == 0
     assert lib.cd_mesh_workspace_bytes(2, 30, 10, 2 ** 30 + 1) == 0      # B * S > 2^31
+    # The backward's chunks (24 B per vertex and chunk when an item has more
+    # than one): about one workgroup per CU, up to two where the chunks then
+    # hold at most 2048 samples, chunk lengths a multiple of 512.
+    assert lib.cd_mesh_workspace_bytes(16, 600, 200, 16384) == 16 * 16 * 600 * 24   # 16 x 1024
+    assert lib.cd_mesh_workspace_bytes(64, 300, 200, 16000) == 64 * 8 * 300 * 24   # 8 x 2048
+    assert lib.cd_mesh_workspace_bytes(4, 3000, 5000, 100000) == 4 * 49 * 3000 * 24  # 2 slices, 49 x 2048
+    assert lib.cd_mesh_workspace_bytes(1, 100, 50, 300000) == (196 * 100 * 24 + 255) // 256 * 256
+    assert lib.cd_mesh_workspace_bytes(600, 50, 30, 3000) == (600 * 30 * 8 + 255) // 256 * 256  # one chunk
     ws = FAKE
     assert lib.cd_mesh_sample_faces(1, 0, 4, FAKE, FAKE, 5, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
     assert lib.cd_mesh_sample_faces(1, 3, 0, FAKE, FAKE, 5, FAKE, FAKE, ws, 1 << 20, None) == CD_ERR_INVALID_ARG
