@@ -336,6 +336,27 @@ def test_extreme_shapes(B, N, M):
     gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), f"B{B}-N{N}-M{M}")
 
 
+@pytest.mark.parametrize("B,N,M", [(100000, 3, 2), (4099, 1, 1), (20000, 17, 40)],
+                         ids=lambda v: str(v))
+def test_many_tiny_items(B, N, M):
+    # The other launch extreme: hundreds of thousands of workgroups of tiny
+    # items in every kernel (forward tiles and merge blocks, metrics, backward
+    # slices); forward bitwise, metrics and backward against the oracle.
+    print(f"[case] many tiny items B={B} N={N} M={M}", flush=True)
+    X, Y = synth.generate("uniform", B, N, M, 47 + N)
+    Xg, Yg = gc.to_gpu(X), gc.to_gpu(Y)
+    dxy, ixy, dyx, iyx = cd.nn_distance(Xg, Yg)
+    g = tuple(gc.to_np(t) for t in (dxy, ixy, dyx, iyx))
+    gc.assert_nn_bitwise(g, oracle.nn(X, Y, fused=True), f"tiny-B{B}")
+    ch, f, p, r = (gc.to_np(t) for t in cd.metrics(dxy, dyx, [0.05, 0.5], 0.75, 1.25))
+    gc.assert_chamfer(ch, g[0], g[2], 0.75, 1.25)
+    for t, tau in enumerate((0.05, 0.5)):
+        gc.assert_fscore(f[t], p[t], r[t], g[0], g[2], tau)
+    go = np.linspace(0.5, 2.0, B).astype(np.float32)
+    gX, gY = cd.chamfer_backward(gc.to_gpu(go), Xg, Yg, ixy, iyx, 0.75, 1.25)
+    gc.assert_grad(gc.to_np(gX), gc.to_np(gY), X, Y, g[1], g[3], go, 0.75, 1.25)
+
+
 BIG_M = (1 << 30) + 3
 BIG_FAR, BIG_MID = BIG_M - 1, 800_000_123
 
