@@ -43,7 +43,7 @@ def _step_tol(eps, nt, cmax, pmax):
 
 
 @pytest.mark.parametrize("B,N,M,eps", [(2, 700, 1300, 0.05), (3, 1100, 513, 0.01), (1, 3000, 3000, 0.2),
-                                       (2, 1, 257, 0.05), (1, 4500, 90, 0.02)])
+                                       (2, 1, 257, 0.05), (1, 4500, 90, 0.02), (1000, 5, 7, 0.05)])
 def test_one_iteration_matches_oracle(B, N, M, eps):
     print(f"[case] emd step B={B} N={N} M={M} eps={eps}", flush=True)
     X, Y = synth.generate("sphere", B, N, M, 7 + N % 5)
