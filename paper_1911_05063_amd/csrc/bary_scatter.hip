@@ -36,6 +36,28 @@ constexpr int64_t kBwdFillGroups = 256;
 constexpr int64_t kBwdMaxGroups = 512;
 constexpr int64_t kBwdHeld = 8;
 
+// Workgroup (b, slice, chunk)'s vertices [v0, v1) of item b (n3 = 3 (v1 - v0)
+// accumulators) and samples [s0, s1); workgroups run chunk-fastest.
+struct Tile {
+    int64_t c, b, v0, v1, s0, s1;
+    int n3;
+};
+
+__device__ __forceinline__ Tile tile_of(int64_t nv, int64_t S, int nslice, int nchunk,
+                                        int64_t chunk)
+{
+    Tile w;
+    w.c = blockIdx.x % nchunk;
+    const int64_t rest = blockIdx.x / nchunk;
+    w.b = rest / nslice;
+    w.v0 = static_cast<int64_t>(rest % nslice) * kVertSlice;
+    w.v1 = std::min<int64_t>(w.v0 + kVertSlice, nv);
+    w.n3 = static_cast<int>(3 * (w.v1 - w.v0));
+    w.s0 = w.c * chunk;
+    w.s1 = std::min<int64_t>(w.s0 + chunk, S);
+    return w;
+}
+
 // Adds sample s's terms w_i * gP[s] to the vertices of face t that lie in the
 // slice [v0, v1) (LDS, fixed point at scale 2^ks); a face with a vertex index
 // outside [0, nv) (t = -1 for a face index out of range) adds nothing.
@@ -95,13 +117,9 @@ __global__ __launch_bounds__(kBwdThreads) void bary_scatter_kernel(
 {
     extern __shared__ unsigned long long acc[];
     __shared__ float red[kBwdThreads / kWave];
-    const int64_t c = blockIdx.x % nchunk;
-    const int64_t rest = blockIdx.x / nchunk;
-    const int64_t b = rest / nslice;
-    const int64_t v0 = static_cast<int64_t>(rest % nslice) * kVertSlice;
-    const int64_t v1 = std::min<int64_t>(v0 + kVertSlice, nv);
-    const int n3 = static_cast<int>(3 * (v1 - v0));
-    const int64_t s0 = c * chunk, s1 = std::min<int64_t>(s0 + chunk, S);
+    const Tile w = tile_of(nv, S, nslice, nchunk, chunk);
+    const int64_t c = w.c, b = w.b, v0 = w.v0, v1 = w.v1, s0 = w.s0, s1 = w.s1;
+    const int n3 = w.n3;
     for (int t = threadIdx.x; t < n3; t += kBwdThreads) acc[t] = 0ull;
     // Scale: every per-vertex sum is bounded by (s1 - s0) * max |gP| because
     // a sample's weights are non-negative and add up to one.
@@ -168,13 +186,9 @@ __global__ __launch_bounds__(kBwdThreads) void bary_scatter_held_kernel(
 {
     extern __shared__ unsigned long long acc[];
     __shared__ float red[kBwdThreads / kWave];
-    const int64_t c = blockIdx.x % nchunk;
-    const int64_t rest = blockIdx.x / nchunk;
-    const int64_t b = rest / nslice;
-    const int64_t v0 = static_cast<int64_t>(rest % nslice) * kVertSlice;
-    const int64_t v1 = std::min<int64_t>(v0 + kVertSlice, nv);
-    const int n3 = static_cast<int>(3 * (v1 - v0));
-    const int64_t s0 = c * chunk, s1 = std::min<int64_t>(s0 + chunk, S);
+    const Tile w = tile_of(nv, S, nslice, nchunk, chunk);
+    const int64_t c = w.c, b = w.b, v0 = w.v0, v1 = w.v1, s0 = w.s0, s1 = w.s1;
+    const int n3 = w.n3;
     // Samples past the chunk's end load its last sample (s1 > s0) and are
     // masked out of the maximum and the sums.
     int32_t f[kPer];
